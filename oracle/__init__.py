@@ -1,0 +1,93 @@
+"""CPU oracle for graph-transformer attention over a CSR graph (float64).
+
+TEST INFRASTRUCTURE: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  The product path
+(the HIP library and its binding) never imports or calls it, and this package
+never imports the product path.
+
+The arithmetic lives in ``gt_oracle.c`` (plain two-pass softmax, per row and
+head, paper Section 2.2 family (iii) with graph-transformer logits).  This
+file only compiles it and marshals numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gt_oracle.c")
+_SO = os.path.join(_HERE, "libgt_oracle.so")
+_lib = None
+
+
+def build() -> str:
+    """Compile gt_oracle.c (always recompiles).  IEEE semantics: no fast-math."""
+    tmp = _SO + ".tmp%d" % os.getpid()
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp,
+                    "-lm"], check=True)
+    os.replace(tmp, _SO)
+    return _SO
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            build()
+        L = ctypes.CDLL(_SO)
+        P = ctypes.c_void_p
+        L.gt_oracle_fwd.argtypes = [ctypes.c_int, P, P, P, P, P, ctypes.c_int64, ctypes.c_int64,
+                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_float, P,
+                                    ctypes.c_int64, P, P, P]
+        L.gt_oracle_fwd.restype = ctypes.c_int
+        L.gt_oracle_threads.argtypes = []
+        L.gt_oracle_threads.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def threads() -> int:
+    return int(_load().gt_oracle_threads())
+
+
+def _ptr(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def gt_attn_fwd(rowptr, colidx, Q, K, V, scale, rows=None, want_absagg=True, want_lse=True):
+    """Reference forward.  Q/K/V: [N,H,D] float32, or uint16 bf16 bit patterns.
+
+    Returns (out, absagg, lse) as float64 arrays shaped [R,H,D], [R,H,D], [R,H]
+    for the requested rows (all rows when ``rows`` is None); absagg/lse are
+    None when not requested.
+    """
+    rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
+    colidx = np.ascontiguousarray(colidx, dtype=np.int32)
+    Q, K, V = (np.ascontiguousarray(x) for x in (Q, K, V))
+    if not (Q.dtype == K.dtype == V.dtype) or Q.dtype not in (np.float32, np.uint16):
+        raise TypeError("Q, K, V must all be float32 or all uint16 (bf16 bits)")
+    if Q.ndim != 3 or K.shape != Q.shape or V.shape != Q.shape:
+        raise ValueError("Q, K, V must share one [N, H, D] shape")
+    N, H, D = Q.shape
+    if rowptr.shape != (N + 1,):
+        raise ValueError("rowptr must have N+1 entries")
+    dtype = 0 if Q.dtype == np.float32 else 1
+    if rows is None:
+        rows_arr, nrows = None, N
+    else:
+        rows_arr = np.ascontiguousarray(rows, dtype=np.int64)
+        nrows = rows_arr.size
+    out = np.empty((nrows, H, D), dtype=np.float64)
+    absagg = np.empty_like(out) if want_absagg else None
+    lse = np.empty((nrows, H), dtype=np.float64) if want_lse else None
+    rc = _load().gt_oracle_fwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K), _ptr(V), N,
+                               colidx.size, H, D, ctypes.c_float(float(scale)), _ptr(rows_arr),
+                               nrows, _ptr(out), _ptr(absagg), _ptr(lse))
+    if rc == 1:
+        raise ValueError("oracle: invalid arguments")
+    if rc == 2:
+        raise ValueError("oracle: invalid CSR structure")
+    return out, absagg, lse

@@ -1,0 +1,88 @@
+"""Shared test helpers: the parity metric and the worked-example loader.
+
+The parity metric compares a result x with the float64 reference r using the
+scale sum_j alpha_ij |v_j| (``absagg``) that bounds the rounding error of any
+floating-point evaluation of a convex combination (Higham, Accuracy and
+Stability of Numerical Algorithms, ch. 4):
+
+    err = max_e |x_e - r_e| / max(|r_e|, absagg_e, tiny)
+
+Where no cancellation happens absagg_e == |r_e| and this is the ordinary
+relative error.
+"""
+from __future__ import annotations
+
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+TOL_F32 = 1e-5
+TOL_BF16 = 2e-2
+
+
+def gate_error(x, ref, absagg) -> float:
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    denom = np.maximum(np.maximum(np.abs(ref), np.asarray(absagg, dtype=np.float64)), 1e-30)
+    if x.size == 0:
+        return 0.0
+    return float(np.max(np.abs(x - ref) / denom))
+
+
+def bf16_bits_to_f32(bits) -> np.ndarray:
+    return (np.asarray(bits).astype(np.uint32) << 16).view(np.float32)
+
+
+def load_worked_example(name: str = "worked_example.txt") -> dict:
+    rows = {}
+    Q, K, V = {}, {}, {}
+    OUT, ABS, LSE = {}, {}, {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            tag, rest = line.split(None, 1)
+            if tag in ("N", "H", "D"):
+                rows[tag] = int(rest)
+            elif tag == "scale":
+                assert rest.strip() == "ln2"
+                rows["scale"] = np.float32(math.log(2.0))
+            elif tag == "rowptr":
+                rows["rowptr"] = np.array([int(t) for t in rest.split()], dtype=np.int64)
+            elif tag == "colidx":
+                rows["colidx"] = np.array([int(t) for t in rest.split()], dtype=np.int32)
+            elif tag in ("Q", "K", "V", "OUT", "ABS", "LSE"):
+                idx, vals = rest.split(None, 1)
+                heads = [h.split() for h in vals.split("|")]
+                tgt = {"Q": Q, "K": K, "V": V, "OUT": OUT, "ABS": ABS, "LSE": LSE}[tag]
+                tgt[int(idx)] = heads
+    N, H, D = rows["N"], rows["H"], rows["D"]
+
+    def arr(d, conv, dtype):
+        a = np.zeros((N, H, D) if d is not LSE else (N, H), dtype=dtype)
+        for i, heads in d.items():
+            for h, vals in enumerate(heads):
+                if d is LSE:
+                    a[i, h] = conv(vals[0])
+                else:
+                    a[i, h, :] = [conv(v) for v in vals]
+        return a
+
+    def lnconv(s):
+        if s == "-inf":
+            return -math.inf
+        assert s.startswith("ln(") and s.endswith(")")
+        return math.log(float(Fraction(s[3:-1])))
+
+    rows["Q"] = arr(Q, float, np.float32)
+    rows["K"] = arr(K, float, np.float32)
+    rows["V"] = arr(V, float, np.float32)
+    rows["OUT"] = arr(OUT, lambda s: float(Fraction(s)), np.float64)
+    rows["ABS"] = arr(ABS, lambda s: float(Fraction(s)), np.float64)
+    rows["LSE"] = arr(LSE, lnconv, np.float64)
+    return rows

@@ -1,0 +1,48 @@
+"""The pins must be able to fail: plant plausible mistakes in copies of the
+oracle source (on the CPU, in a temporary directory) and check that the pin
+suite rejects every one of them."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "gt_oracle.c")
+
+MUTANTS = {
+    "no_max_shift": ("const double w = exp(s[t] - m);", "const double w = exp(s[t]);"),
+    "transposed_roles": (
+        "elem(Q, dtype, (i * H + h) * (int64_t)D + d) *\n"
+        "                           elem(K, dtype, (j * H + h) * (int64_t)D + d)",
+        "elem(Q, dtype, (j * H + h) * (int64_t)D + d) *\n"
+        "                           elem(K, dtype, (i * H + h) * (int64_t)D + d)"),
+    "no_scale": ("s[t] = (double)scale * dot;", "s[t] = dot;"),
+    "sign_flip": ("s[t] = (double)scale * dot;", "s[t] = -(double)scale * dot;"),
+    "row_end_off_by_one": ("const int64_t deg = e - b;",
+                           "const int64_t deg = e - b > 0 ? e - b - 1 : 0;"),
+    "wrong_head_for_v": ("const double v = elem(V, dtype, (j * H + h) * (int64_t)D + d);",
+                         "const double v = elem(V, dtype, (j * H + 0) * (int64_t)D + d);"),
+    "lse_drops_max": ("lse[r * H + h] = m + log(Z);", "lse[r * H + h] = log(Z);"),
+    "absagg_signed": ("if (a) a[d] += w * fabs(v);", "if (a) a[d] += w * v;"),
+    "bf16_widening": ("uint32_t bits = (uint32_t)((const uint16_t*)base)[k] << 16;",
+                      "uint32_t bits = (uint32_t)((const uint16_t*)base)[k] << 15;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_mutant(name, tmp_path):
+    src = open(SRC).read()
+    old, new = MUTANTS[name]
+    assert old in src, "mutation site moved: update the mutant table"
+    csrc = tmp_path / "gt_oracle.c"
+    csrc.write_text(src.replace(old, new))
+    so = tmp_path / "libgt_oracle.so"
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", str(csrc), "-o",
+                    str(so), "-lm"], check=True)
+    code = ("import sys, oracle, pytest; oracle._SO = %r; "
+            "sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider', %r]))"
+            % (str(so), os.path.join(ROOT, "tests", "test_oracle_pins.py")))
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                       env=dict(os.environ, OMP_NUM_THREADS="2"))
+    assert r.returncode != 0, "pins accepted a planted mistake: " + name
