@@ -1,0 +1,152 @@
+/*
+ * gt_attn.h -- fused graph-transformer attention forward over a CSR graph,
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Operation (paper: Section 2.2, attention-based family (iii) with the
+ * graph-transformer logits e_ij = q_i . k_j / sqrt(D); fused single-pass
+ * evaluation: Section 3.2 and Appendix D.2, "Fused forward in CSR" and
+ * "Online softmax and fused aggregation"):
+ *
+ *   for every destination row i in [0, N) and head h in [0, H):
+ *     s_e           = scale * sum_d Q[i,h,d] * K[j_e,h,d]   for each CSR entry e of row i,
+ *                                                           j_e = colidx[e]
+ *     out[i,h,:]    = sum_e softmax_e(s) * V[j_e,h,:]
+ *
+ *   Every CSR entry is one softmax term (a repeated entry counts twice); no
+ *   self-loop is added beyond what the CSR lists.  A row with no entries
+ *   yields out[i,h,:] = 0.  Scores, probabilities and per-edge messages are
+ *   never written to memory: each row is streamed once with a running
+ *   (max, sum, accumulator) state, and partial states of split rows are
+ *   merged by rescaling with exp(m_part - m_total) (Appendix D.2, "Cross-warp
+ *   merge and normalization").
+ *
+ * Layouts (all row-major, dense):
+ *   rowptr  int64  [N+1]   rowptr[0] = 0, non-decreasing, rowptr[N] = E
+ *   colidx  int32  [E]     source ids in [0, N); rows need not be sorted
+ *   Q, K, V, out  [N][H][D] elements; fp32, or bf16 as raw uint16 bit patterns
+ *
+ * Precision: loads fp32 or bf16 (bf16 is widened exactly), accumulates in
+ * fp32, exponentials in base 2 on a log2(e)-prescaled score; bf16 outputs
+ * are rounded to nearest even from the fp32 result.
+ *
+ * Ownership and memory: every pointer argument is DEVICE memory owned by the
+ * caller; the library neither frees nor retains it past the enqueued work.
+ * `out` must not overlap Q, K or V.  Q, K, V and out must be 16-byte aligned.
+ * Temporary workspace is allocated stream-ordered on `stream`
+ * (hipMallocAsync / hipFreeAsync) and released when the call's work ends.
+ *
+ * Semantics: asynchronous.  GT_SUCCESS means the work was enqueued on
+ * `stream`; device faults surface at the caller's next synchronisation.
+ * N == 0 enqueues nothing.  The CSR structure is a precondition (checked by
+ * gt_csr_validate, never on this path); a malformed CSR is undefined behaviour.
+ *
+ * Errors: arguments are validated on the host before any device work;
+ * failures return a gt_status and set a thread-local message readable with
+ * gt_last_error_message().  Validation never reads device memory.
+ *
+ * Supported shapes: H in {1, 2, 4, 8}, D in {32, 64, 128}; 0 <= E < 2^31;
+ * 0 <= N < 2^31.
+ */
+#ifndef GT_ATTN_H
+#define GT_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gt_status {
+    GT_SUCCESS = 0,
+    GT_ERROR_INVALID_VALUE = 1, /* null pointer, bad size, misalignment, aliasing, non-finite scale */
+    GT_ERROR_NOT_SUPPORTED = 2, /* (H, D) or dtype outside the compiled set */
+    GT_ERROR_OUT_OF_MEMORY = 3, /* workspace allocation failed */
+    GT_ERROR_HIP = 4            /* a HIP runtime call or kernel launch failed */
+} gt_status;
+
+typedef enum gt_dtype {
+    GT_DTYPE_F32 = 0,
+    GT_DTYPE_BF16 = 1
+} gt_dtype;
+
+/*
+ * fp32 features.  out[i,h,:] as defined above.  scale is typically 1/sqrt(D)
+ * (the paper's logit scaling, Section 2.2) and must be finite.
+ */
+gt_status gt_attn_fwd(const int64_t* rowptr, const int32_t* colidx, const float* Q,
+                      const float* K, const float* V, float* out, int64_t N, int64_t E,
+                      int32_t H, int32_t D, float scale, hipStream_t stream);
+
+/*
+ * bf16 features given as uint16 bit patterns; fp32 accumulation; bf16 output
+ * rounded to nearest even.  Otherwise identical to gt_attn_fwd.
+ */
+gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const uint16_t* Q,
+                           const uint16_t* K, const uint16_t* V, uint16_t* out, int64_t N,
+                           int64_t E, int32_t H, int32_t D, float scale, hipStream_t stream);
+
+/*
+ * Work-partition overrides (Appendix B.1 and D.1: degree-aware allocation of
+ * rows to wavefronts, with light/heavy thresholds and per-chunk edge counts
+ * that the paper tunes by grid search).  A field <= 0 selects the default.
+ *   light_max_deg : rows of degree <= this are handled by one lane group
+ *                   (a sub-wavefront) each
+ *   heavy_min_deg : rows of degree >= this are split into chunks processed
+ *                   by different wavefronts and merged afterwards; rows in
+ *                   between get one wavefront each
+ *   chunk_edges   : CSR entries per chunk of a split row (rounded up to a
+ *                   multiple of 64)
+ *   grid_blocks   : workgroups of the persistent attention kernel (rounded
+ *                   up to a multiple of 8)
+ * Results are bitwise reproducible for fixed settings; different settings
+ * change only the fp32 rounding.
+ */
+typedef struct gt_tuning {
+    int32_t light_max_deg;
+    int32_t heavy_min_deg;
+    int32_t chunk_edges;
+    int32_t grid_blocks;
+} gt_tuning;
+
+/*
+ * Generic entry: dtype selects fp32 (void* = float*) or bf16 (void* =
+ * uint16_t*); tuning may be NULL (defaults).  Same contract as gt_attn_fwd.
+ */
+gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx,
+                         const void* Q, const void* K, const void* V, void* out, int64_t N,
+                         int64_t E, int32_t H, int32_t D, float scale, const gt_tuning* tuning,
+                         hipStream_t stream);
+
+/*
+ * Debug utility, never on the attention path: checks on the device that
+ * rowptr[0] == 0, rowptr is non-decreasing, rowptr[N] == E and every colidx
+ * entry lies in [0, N).  Synchronous on `stream`; *valid (host memory) is set
+ * to 1 for a well-formed CSR, else 0.
+ */
+gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t N, int64_t E,
+                          int32_t* valid, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* gt_status_string(gt_status status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* gt_last_error_message(void);
+
+/*
+ * Kernel timing for benchmarking.  While enabled, every attention call
+ * records HIP events on its stream around its three phases: [0] partition
+ * (counter reset + degree binning), [1] the attention kernel, [2] the merge of
+ * split rows.  gt_profile_collect waits for the recorded events, adds their
+ * elapsed milliseconds into ms[0..2], sets *calls, and clears the record.
+ * Enabling or disabling also clears it.  Process-wide, thread-safe.
+ */
+gt_status gt_profile_enable(int32_t enable);
+gt_status gt_profile_collect(double ms[3], int64_t* calls);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GT_ATTN_H */

@@ -1,0 +1,175 @@
+"""Fused graph-transformer attention over a CSR graph for AMD MI355X (gfx950).
+
+Python binding of the C ABI declared in ``include/gt_attn.h``.  Every function
+here only marshals arguments (torch tensors -> device pointers, sizes and the
+current HIP stream) and calls ``libgtattn.so``; all arithmetic runs in the HIP
+kernels.  PyTorch provides device memory and streams.  There is no fallback:
+if the library is missing or the call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgtattn.so")
+
+GT_SUCCESS = 0
+GT_ERROR_INVALID_VALUE = 1
+GT_ERROR_NOT_SUPPORTED = 2
+GT_ERROR_OUT_OF_MEMORY = 3
+GT_ERROR_HIP = 4
+GT_DTYPE_F32 = 0
+GT_DTYPE_BF16 = 1
+
+EXPORTED_SYMBOLS = (
+    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_csr_validate", "gt_status_string",
+    "gt_last_error_message", "gt_profile_enable", "gt_profile_collect",
+)
+
+
+class GtTuning(ctypes.Structure):
+    _fields_ = [("light_max_deg", ctypes.c_int32), ("heavy_min_deg", ctypes.c_int32),
+                ("chunk_edges", ctypes.c_int32), ("grid_blocks", ctypes.c_int32)]
+
+
+class GtError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("gt_attn status %d: %s" % (status, message))
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libgtattn.so (torch is imported first so the library binds to the
+    HIP runtime torch already loaded, making torch streams valid for it)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libgtattn.so is not built; run __graft_entry__.build() or "
+                           "python -m paper_2605_31500_amd._build")
+    L = ctypes.CDLL(path)
+    P, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float
+    sig = [P, P, P, P, P, P, i64, i64, i32, i32, f32, P]
+    L.gt_attn_fwd.argtypes = sig
+    L.gt_attn_fwd_bf16.argtypes = sig
+    L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:-1] + [ctypes.POINTER(GtTuning), P]
+    L.gt_csr_validate.argtypes = [P, P, i64, i64, ctypes.POINTER(i32), P]
+    L.gt_status_string.argtypes = [ctypes.c_int]
+    L.gt_status_string.restype = ctypes.c_char_p
+    L.gt_last_error_message.argtypes = []
+    L.gt_last_error_message.restype = ctypes.c_char_p
+    L.gt_profile_enable.argtypes = [i32]
+    L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
+    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_csr_validate",
+                 "gt_profile_enable", "gt_profile_collect"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != GT_SUCCESS:
+        L = load_library()
+        raise GtError(status, "%s: %s" % (L.gt_status_string(status).decode(),
+                                         L.gt_last_error_message().decode()))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device, stream):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check_tensors(rowptr, colidx, Q, K, V, out, dtypes):
+    for name, t in (("rowptr", rowptr), ("colidx", colidx), ("Q", Q), ("K", K), ("V", V),
+                    ("out", out)):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(name + " must be a torch.Tensor")
+        if not t.is_cuda:
+            raise ValueError(name + " must be a device tensor")
+        if not t.is_contiguous():
+            raise ValueError(name + " must be contiguous")
+    if rowptr.dtype != torch.int64 or colidx.dtype != torch.int32:
+        raise TypeError("rowptr must be int64 and colidx int32")
+    if Q.dim() != 3 or K.shape != Q.shape or V.shape != Q.shape or out.shape != Q.shape:
+        raise ValueError("Q, K, V, out must share one [N, H, D] shape")
+    for t in (Q, K, V, out):
+        if t.dtype not in dtypes:
+            raise TypeError("feature dtype %s not in %s" % (t.dtype, dtypes))
+    if rowptr.numel() != Q.shape[0] + 1:
+        raise ValueError("rowptr must have N+1 entries")
+
+
+def gt_attn_fwd(rowptr, colidx, Q, K, V, out, scale, stream=None) -> None:
+    """fp32 features; writes out.  See include/gt_attn.h."""
+    _check_tensors(rowptr, colidx, Q, K, V, out, (torch.float32,))
+    N, H, D = Q.shape
+    _check(load_library().gt_attn_fwd(_ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K), _ptr(V),
+                                      _ptr(out), N, colidx.numel(), H, D, float(scale),
+                                      _stream(Q.device, stream)))
+
+
+def gt_attn_fwd_bf16(rowptr, colidx, Q, K, V, out, scale, stream=None) -> None:
+    """bf16 features (torch.bfloat16, or int16/uint16 holding bf16 bits); writes out."""
+    _check_tensors(rowptr, colidx, Q, K, V, out, (torch.bfloat16, torch.int16, torch.uint16))
+    N, H, D = Q.shape
+    _check(load_library().gt_attn_fwd_bf16(_ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K), _ptr(V),
+                                           _ptr(out), N, colidx.numel(), H, D, float(scale),
+                                           _stream(Q.device, stream)))
+
+
+def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None) -> None:
+    """Either dtype (taken from Q); tuning: dict or GtTuning of partition overrides."""
+    if Q.dtype == torch.float32:
+        dtype, allowed = GT_DTYPE_F32, (torch.float32,)
+    else:
+        dtype, allowed = GT_DTYPE_BF16, (torch.bfloat16, torch.int16, torch.uint16)
+    _check_tensors(rowptr, colidx, Q, K, V, out, allowed)
+    N, H, D = Q.shape
+    if isinstance(tuning, dict):
+        tuning = GtTuning(**tuning)
+    tp = ctypes.byref(tuning) if tuning is not None else None
+    _check(load_library().gt_attn_fwd_ex(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
+                                         _ptr(V), _ptr(out), N, colidx.numel(), H, D,
+                                         float(scale), tp, _stream(Q.device, stream)))
+
+
+def attention(rowptr, colidx, Q, K, V, scale=None, tuning=None, out=None, stream=None):
+    """Convenience: allocates ``out`` like Q and dispatches on Q's dtype."""
+    if out is None:
+        out = torch.empty_like(Q)
+    if scale is None:
+        scale = Q.shape[-1] ** -0.5
+    gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=tuning, stream=stream)
+    return out
+
+
+def gt_csr_validate(rowptr, colidx, stream=None) -> bool:
+    """Device-side CSR structure check (synchronous)."""
+    valid = ctypes.c_int32(0)
+    _check(load_library().gt_csr_validate(_ptr(rowptr), _ptr(colidx), rowptr.numel() - 1,
+                                          colidx.numel(), ctypes.byref(valid),
+                                          _stream(rowptr.device, stream)))
+    return bool(valid.value)
+
+
+def gt_profile_enable(enable: bool = True) -> None:
+    _check(load_library().gt_profile_enable(1 if enable else 0))
+
+
+def gt_profile_collect():
+    """Returns ([partition_ms, attention_ms, merge_ms] summed over calls, calls)."""
+    ms = (ctypes.c_double * 3)()
+    calls = ctypes.c_int64(0)
+    _check(load_library().gt_profile_collect(ms, ctypes.byref(calls)))
+    return [ms[0], ms[1], ms[2]], calls.value

@@ -1,0 +1,897 @@
+// Fused graph-transformer attention forward over a CSR graph, for gfx950.
+//
+// Operation: paper Section 2.2, attention family (iii) with graph-transformer
+// logits; single streaming pass with online softmax (Section 3.2, Appendix
+// D.2).  For every destination row i and head h:
+//     out[i,h,:] = sum_e softmax_e(scale * <Q[i,h,:], K[j_e,h,:]>) V[j_e,h,:]
+//
+// Mapping (designed for 64-wide wavefronts, not taken from the paper's
+// one-block-per-(node, head) CUDA layout):
+//   * A node row of all heads, H*D elements, is R = H*D*sizeof(T) contiguous
+//     bytes.  A lane group of G = min(64, R/16) lanes covers it with one
+//     16-byte load per lane (NV = R/(16*G) loads when R > 1 KiB), so every
+//     gathered K/V row is one fully coalesced request, and a wave holds
+//     P = 64/G independent groups.
+//   * A head's D elements occupy HL = D*sizeof(T)/16 consecutive lanes; the
+//     score of a head is reduced across those lanes with DPP lane swaps.
+//   * Degree-aware work split (Appendix B.1; Appendix D.1 for the chunked
+//     heavy-node scheme): light rows get one group each, medium rows one wave
+//     (the P groups split the row's entries and are merged across lanes),
+//     heavy rows are cut into chunks processed by different waves whose
+//     partial (max, sum, acc) states are merged in chunk order by a second
+//     kernel, so results are bitwise reproducible and need no float atomics.
+//   * Each group processes U entries per step: all U K-row and V-row loads
+//     are issued before any is consumed, then one online-softmax update
+//     covers the U entries (one rescale per step instead of one per entry).
+//   * Neighbour indices are staged in LDS tiles loaded with one coalesced
+//     4-byte load per lane.
+//   * Light rows are assigned XCD-contiguously: the workgroups resident on
+//     one XCD process one contiguous range of rows, so rows with shared
+//     neighbourhoods (community-ordered ids) share that XCD's L2.
+
+#include <hip/hip_runtime.h>
+
+#include <array>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "gt_attn.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+constexpr int kXcds = 8;
+
+// Counter slots in the workspace (reset to zero at the start of each call).
+enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_WORDS = 16 };
+
+struct bf16_tag {};
+
+template <typename T> struct Elt;
+template <> struct Elt<float> { static constexpr int kBytes = 4; };
+template <> struct Elt<bf16_tag> { static constexpr int kBytes = 2; };
+
+template <typename T, int H, int D>
+struct Geo {
+    static constexpr int kEB = Elt<T>::kBytes;
+    static constexpr int kEPV = 16 / kEB;                   // elements per 16-B vector
+    static constexpr int kRowBytes = H * D * kEB;           // one node row, all heads
+    static constexpr int kNVec = kRowBytes / 16;
+    static constexpr int kG = kNVec < kWave ? kNVec : kWave;  // lanes per group
+    static constexpr int kNV = kNVec / kG;                  // 16-B vectors per lane
+    static constexpr int kP = kWave / kG;                   // groups per wave
+    static constexpr int kHL = D * kEB / 16;                // lanes per head (per vector slot)
+    static constexpr int kU0 = (8 / kNV) > 2 ? (8 / kNV) : 2;
+    static constexpr int kU = kU0 < kG ? kU0 : kG;          // entries per step per group
+    static constexpr int kHD = H * D;
+    static_assert(kRowBytes % 16 == 0, "row must be a whole number of 16-B vectors");
+    static_assert(kHL >= 1 && kG % kHL == 0, "heads must tile the lane group");
+    static_assert(kG % kU == 0 && kP * kU <= kWave, "index tiles must cover whole steps");
+};
+
+struct ChunkItem {
+    int32_t row;
+    int32_t slot;
+    int64_t begin;
+    int64_t end;
+};
+
+struct HeavyRow {
+    int32_t row;
+    int32_t base;  // first partial slot
+    int32_t nch;   // number of chunks
+    int32_t pad;
+};
+
+struct AttnParams {
+    const int64_t* rowptr;
+    const int32_t* colidx;
+    const char* Q;
+    const char* K;
+    const char* V;
+    char* out;
+    int64_t N;
+    float c;  // scale * log2(e)
+    int32_t light_max;
+    int32_t cap_chunks;
+    const int32_t* counters;
+    const int32_t* med_list;
+    const ChunkItem* chunks;
+    float* part_acc;   // [slot][H*D]
+    float2* part_ml;   // [slot][H]: (running max in log2 units, sum)
+};
+
+struct PartParams {
+    const int64_t* rowptr;
+    int64_t N;
+    int32_t light_max;
+    int32_t heavy_min;
+    int32_t chunk;
+    int32_t cap_heavy;
+    int32_t cap_chunks;
+    int32_t* counters;
+    int32_t* med_list;
+    HeavyRow* heavy;
+    ChunkItem* chunks;
+};
+
+struct MergeParams {
+    int32_t cap_heavy;
+    const int32_t* counters;
+    const HeavyRow* heavy;
+    const float* part_acc;
+    const float2* part_ml;
+    char* out;
+};
+
+// ------------------------------------------------------------ element codecs
+
+template <typename T> __device__ __forceinline__ void widen(const uint4& r, float* f);
+
+template <> __device__ __forceinline__ void widen<float>(const uint4& r, float* f) {
+    f[0] = __uint_as_float(r.x);
+    f[1] = __uint_as_float(r.y);
+    f[2] = __uint_as_float(r.z);
+    f[3] = __uint_as_float(r.w);
+}
+
+// bf16 element 2k sits in the low half of dword k (little endian); widening
+// places the 16 bits in the upper half of an fp32 word, which is exact.
+template <> __device__ __forceinline__ void widen<bf16_tag>(const uint4& r, float* f) {
+    f[0] = __uint_as_float(r.x << 16);
+    f[1] = __uint_as_float(r.x & 0xFFFF0000u);
+    f[2] = __uint_as_float(r.y << 16);
+    f[3] = __uint_as_float(r.y & 0xFFFF0000u);
+    f[4] = __uint_as_float(r.z << 16);
+    f[5] = __uint_as_float(r.z & 0xFFFF0000u);
+    f[6] = __uint_as_float(r.w << 16);
+    f[7] = __uint_as_float(r.w & 0xFFFF0000u);
+}
+
+// fp32 -> bf16 bits, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <typename T> __device__ __forceinline__ uint4 narrow(const float* f);
+
+template <> __device__ __forceinline__ uint4 narrow<float>(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                      __float_as_uint(f[3]));
+}
+
+template <> __device__ __forceinline__ uint4 narrow<bf16_tag>(const float* f) {
+    return make_uint4(bf16_rne(f[0]) | (bf16_rne(f[1]) << 16), bf16_rne(f[2]) | (bf16_rne(f[3]) << 16),
+                      bf16_rne(f[4]) | (bf16_rne(f[5]) << 16), bf16_rne(f[6]) | (bf16_rne(f[7]) << 16));
+}
+
+// ---------------------------------------------------------- cross-lane sums
+
+template <int CTRL> __device__ __forceinline__ float dpp(float x) {
+    return __builtin_amdgcn_update_dpp(0.0f, x, CTRL, 0xF, 0xF, false);
+}
+
+// Sum over aligned groups of HL lanes; every lane of a group ends with the
+// same bits (each step adds a pair of values in both orders, a+b == b+a).
+template <int HL> __device__ __forceinline__ float head_sum(float x) {
+    if constexpr (HL >= 2) x += dpp<0xB1>(x);    // quad_perm [1,0,3,2]: lane ^ 1
+    if constexpr (HL >= 4) x += dpp<0x4E>(x);    // quad_perm [2,3,0,1]: lane ^ 2
+    if constexpr (HL >= 8) x += dpp<0x141>(x);   // row_half_mirror: other quad of 8
+    if constexpr (HL >= 16) x += dpp<0x140>(x);  // row_mirror: other half of 16
+    if constexpr (HL >= 32) x += __shfl_xor(x, 16);
+    if constexpr (HL >= 64) x += __shfl_xor(x, 32);
+    return x;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Orders LDS traffic of one wavefront around a tile hand-off (the hardware
+// executes a wave's LDS operations in order; this stops compiler reordering).
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// ------------------------------------------------------------ per-lane state
+
+template <typename T, int H, int D>
+struct RowState {
+    using Gm = Geo<T, H, D>;
+    float q[Gm::kNV][Gm::kEPV];
+    float acc[Gm::kNV][Gm::kEPV];
+    float m[Gm::kNV];  // running max of log2-scaled scores for this lane's head
+    float l[Gm::kNV];  // running sum of 2^(s - m)
+
+    __device__ __forceinline__ void begin(const char* __restrict__ Qb, int64_t row, int lig) {
+        const char* qrow = Qb + row * (int64_t)Gm::kRowBytes + lig * 16;
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            const uint4 r = *reinterpret_cast<const uint4*>(qrow + k * Gm::kG * 16);
+            widen<T>(r, q[k]);
+            m[k] = -INFINITY;
+            l[k] = 0.0f;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = 0.0f;
+        }
+    }
+
+    // One step over U entries (indices j[0..U)); entries u >= nvalid are
+    // copies of valid indices and contribute nothing (score -inf).
+    __device__ __forceinline__ void step(const char* __restrict__ Kb, const char* __restrict__ Vb,
+                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c) {
+        // No implicit contraction: fusing the score product into the later
+        // subtraction of the running max would give the maximal entry a weight
+        // of 2^(rounding error) instead of exactly 1.
+#pragma clang fp contract(off)
+        constexpr int U = Gm::kU;
+        uint4 kr[U][Gm::kNV], vr[U][Gm::kNV];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t off = (int64_t)j[u] * Gm::kRowBytes + lig * 16;
+#pragma unroll
+            for (int k = 0; k < Gm::kNV; ++k) {
+                kr[u][k] = *reinterpret_cast<const uint4*>(Kb + off + k * Gm::kG * 16);
+                vr[u][k] = *reinterpret_cast<const uint4*>(Vb + off + k * Gm::kG * 16);
+            }
+        }
+        float s[U][Gm::kNV];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int k = 0; k < Gm::kNV; ++k) {
+                float kf[Gm::kEPV];
+                widen<T>(kr[u][k], kf);
+                float d = 0.0f;
+#pragma unroll
+                for (int e = 0; e < Gm::kEPV; ++e) d = fmaf(q[k][e], kf[e], d);
+                d = head_sum<Gm::kHL>(d) * c;
+                s[u][k] = (u < nvalid) ? d : -INFINITY;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            float mb = m[k];
+#pragma unroll
+            for (int u = 0; u < U; ++u) mb = fmaxf(mb, s[u][k]);
+            const float corr = fast_exp2(m[k] - mb);  // 0 on the first step (m = -inf)
+            l[k] *= corr;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] *= corr;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const float pu = fast_exp2(s[u][k] - mb);
+                l[k] += pu;
+                float vf[Gm::kEPV];
+                widen<T>(vr[u][k], vf);
+#pragma unroll
+                for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = fmaf(pu, vf[e], acc[k][e]);
+            }
+            m[k] = mb;
+        }
+    }
+
+    // Merge the state held by the lane `off` positions away (same vector
+    // slots in another group of the wave).
+    __device__ __forceinline__ void merge_xor(int off) {
+#pragma clang fp contract(off)
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            const float mo = __shfl_xor(m[k], off);
+            const float lo = __shfl_xor(l[k], off);
+            const float mn = fmaxf(m[k], mo);
+            const float ca = (m[k] == mn) ? 1.0f : fast_exp2(m[k] - mn);
+            const float cb = (mo == mn) ? 1.0f : fast_exp2(mo - mn);
+            l[k] = l[k] * ca + lo * cb;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) {
+                const float ao = __shfl_xor(acc[k][e], off);
+                acc[k][e] = acc[k][e] * ca + ao * cb;
+            }
+            m[k] = mn;
+        }
+    }
+
+    __device__ __forceinline__ void store_out(char* __restrict__ outb, int64_t row, int lig) const {
+        char* orow = outb + row * (int64_t)Gm::kRowBytes + lig * 16;
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            const float inv = l[k] > 0.0f ? 1.0f / l[k] : 0.0f;
+            float o[Gm::kEPV];
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) o[e] = acc[k][e] * inv;
+            *reinterpret_cast<uint4*>(orow + k * Gm::kG * 16) = narrow<T>(o);
+        }
+    }
+
+    __device__ __forceinline__ void store_partial(float* __restrict__ pacc, float2* __restrict__ pml,
+                                                  int32_t slot, int lig) const {
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            const int v = lig + k * Gm::kG;  // vector index within the row
+            float* dst = pacc + (int64_t)slot * Gm::kHD + v * Gm::kEPV;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; e += 4)
+                *reinterpret_cast<float4*>(dst + e) =
+                    make_float4(acc[k][e], acc[k][e + 1], acc[k][e + 2], acc[k][e + 3]);
+            if (v % Gm::kHL == 0) pml[(int64_t)slot * H + v / Gm::kHL] = make_float2(m[k], l[k]);
+        }
+    }
+};
+
+// One wavefront streams CSR entries [b, e) of `row`; slot < 0 writes the
+// normalised output, slot >= 0 writes the partial state of a chunk.
+template <typename T, int H, int D>
+__device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, int64_t b, int64_t e,
+                                             int32_t slot, int32_t* __restrict__ tile, int lane) {
+    using Gm = Geo<T, H, D>;
+    constexpr int U = Gm::kU, P = Gm::kP, G = Gm::kG;
+    const int g = lane / G, lig = lane % G;
+    RowState<T, H, D> st;
+    st.begin(p.Q, row, lig);
+    for (int64_t tb = b; tb < e; tb += kWave) {
+        const int64_t pos = (tb + lane < e) ? tb + lane : e - 1;
+        const int32_t idx = p.colidx[pos];
+        wave_lds_fence();
+        tile[lane] = idx;
+        wave_lds_fence();
+        const int nt = (int)((e - tb) < kWave ? (e - tb) : kWave);
+        for (int t = 0; t < nt; t += P * U) {
+            const int e0 = t + g * U;
+            const int nvalid = nt - e0 < U ? nt - e0 : U;
+            if (nvalid > 0) {
+                int32_t j[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) j[u] = tile[e0 + u];
+                st.step(p.K, p.V, j, nvalid, lig, p.c);
+            }
+        }
+    }
+#pragma unroll
+    for (int off = G; off < kWave; off <<= 1) st.merge_xor(off);
+    if (g == 0) {
+        if (slot < 0)
+            st.store_out(p.out, row, lig);
+        else
+            st.store_partial(p.part_acc, p.part_ml, slot, lig);
+    }
+}
+
+// One lane group handles a whole light row (degree <= light_max).
+template <typename T, int H, int D>
+__device__ __forceinline__ void group_row(const AttnParams& p, int64_t row, int32_t* __restrict__ gtile,
+                                          int lig) {
+    using Gm = Geo<T, H, D>;
+    constexpr int U = Gm::kU, G = Gm::kG;
+    if (row >= p.N) return;
+    const int64_t b = p.rowptr[row], e = p.rowptr[row + 1];
+    if (e - b > p.light_max) return;
+    RowState<T, H, D> st;
+    st.begin(p.Q, row, lig);
+    for (int64_t tb = b; tb < e; tb += G) {
+        const int64_t pos = (tb + lig < e) ? tb + lig : e - 1;
+        const int32_t idx = p.colidx[pos];
+        wave_lds_fence();
+        gtile[lig] = idx;
+        wave_lds_fence();
+        const int nt = (int)((e - tb) < G ? (e - tb) : G);
+        for (int t = 0; t < nt; t += U) {
+            const int nvalid = nt - t < U ? nt - t : U;
+            int32_t j[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) j[u] = gtile[t + u];
+            st.step(p.K, p.V, j, nvalid, lig, p.c);
+        }
+    }
+    st.store_out(p.out, row, lig);
+}
+
+// Persistent attention kernel: first the chunk items (pieces of heavy rows,
+// then whole medium rows), one wavefront each; then the light rows, P per
+// wavefront, in XCD-contiguous ranges.
+template <typename T, int H, int D>
+__global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
+    using Gm = Geo<T, H, D>;
+    __shared__ int32_t tiles[kWavesPerBlock][kWave];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x / kWave;
+    int32_t* tile = tiles[wv];
+
+    // Counts come from the partition kernel; clamping keeps every list read
+    // inside the workspace even if the CSR precondition were violated.
+    const int32_t n_chunks = min(p.counters[CNT_CHUNKS], p.cap_chunks);
+    const int32_t n_items = n_chunks + (int32_t)min((int64_t)p.counters[CNT_MED], p.N);
+    const int nwaves = gridDim.x * kWavesPerBlock;
+    for (int it = blockIdx.x * kWavesPerBlock + wv; it < n_items; it += nwaves) {
+        if (it < n_chunks) {
+            const ChunkItem ci = p.chunks[it];
+            wave_segment<T, H, D>(p, ci.row, ci.begin, ci.end, ci.slot, tile, lane);
+        } else {
+            const int64_t row = p.med_list[it - n_chunks];
+            wave_segment<T, H, D>(p, row, p.rowptr[row], p.rowptr[row + 1], -1, tile, lane);
+        }
+    }
+
+    const int xcd = blockIdx.x % kXcds;
+    const int waves_per_xcd = (gridDim.x / kXcds) * kWavesPerBlock;
+    const int lw = (blockIdx.x / kXcds) * kWavesPerBlock + wv;
+    const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
+    const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
+    const int g = lane / Gm::kG, lig = lane % Gm::kG;
+    for (int64_t it = lo + lw; it < hi; it += waves_per_xcd)
+        group_row<T, H, D>(p, it * Gm::kP + g, tile + g * Gm::kG, lig);
+}
+
+// Degree binning.  Each block owns a contiguous range of rows; per-thread
+// counts are scanned inside the block and one atomic per list reserves the
+// block's output range.
+constexpr int kPartRowsPerThread = 8;
+constexpr int kPartRowsPerBlock = kBlock * kPartRowsPerThread;
+
+__device__ __forceinline__ int block_exclusive_scan(int v, int* lds_waves, int* total) {
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) lds_waves[wv] = x;
+    __syncthreads();
+    int before = 0, sum = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+        if (w < wv) before += lds_waves[w];
+        sum += lds_waves[w];
+    }
+    __syncthreads();
+    *total = sum;
+    return before + x - v;
+}
+
+__global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
+    __shared__ int lds[3][kWavesPerBlock];
+    __shared__ int base[3];
+    const int64_t r0 = (int64_t)blockIdx.x * kPartRowsPerBlock + (int64_t)threadIdx.x * kPartRowsPerThread;
+    int n_med = 0, n_heavy = 0, n_chunk = 0;
+    int64_t deg[kPartRowsPerThread];
+#pragma unroll
+    for (int t = 0; t < kPartRowsPerThread; ++t) {
+        const int64_t r = r0 + t;
+        deg[t] = (r < p.N) ? p.rowptr[r + 1] - p.rowptr[r] : 0;
+        if (deg[t] >= p.heavy_min) {
+            ++n_heavy;
+            n_chunk += (int)((deg[t] + p.chunk - 1) / p.chunk);
+        } else if (deg[t] > p.light_max) {
+            ++n_med;
+        }
+    }
+    int tot_med, tot_heavy, tot_chunk;
+    const int off_med = block_exclusive_scan(n_med, lds[0], &tot_med);
+    const int off_heavy = block_exclusive_scan(n_heavy, lds[1], &tot_heavy);
+    const int off_chunk = block_exclusive_scan(n_chunk, lds[2], &tot_chunk);
+    if (threadIdx.x == 0) {
+        base[0] = tot_med ? atomicAdd(&p.counters[CNT_MED], tot_med) : 0;
+        base[1] = tot_heavy ? atomicAdd(&p.counters[CNT_HEAVY], tot_heavy) : 0;
+        base[2] = tot_chunk ? atomicAdd(&p.counters[CNT_CHUNKS], tot_chunk) : 0;
+    }
+    __syncthreads();
+    int im = base[0] + off_med, ih = base[1] + off_heavy, ic = base[2] + off_chunk;
+#pragma unroll
+    for (int t = 0; t < kPartRowsPerThread; ++t) {
+        const int64_t r = r0 + t;
+        if (r >= p.N) break;
+        if (deg[t] >= p.heavy_min) {
+            const int nch = (int)((deg[t] + p.chunk - 1) / p.chunk);
+            if (ih >= p.cap_heavy || ic + nch > p.cap_chunks) {
+                atomicOr(&p.counters[CNT_OVERFLOW], 1);
+            } else {
+                const int64_t b = p.rowptr[r];
+                p.heavy[ih] = HeavyRow{(int32_t)r, ic, nch, 0};
+                for (int c = 0; c < nch; ++c) {
+                    const int64_t cb = b + (int64_t)c * p.chunk;
+                    const int64_t ce = (cb + p.chunk < b + deg[t]) ? cb + p.chunk : b + deg[t];
+                    p.chunks[ic + c] = ChunkItem{(int32_t)r, ic + c, cb, ce};
+                }
+            }
+            ++ih;
+            ic += nch;
+        } else if (deg[t] > p.light_max) {
+            p.med_list[im++] = (int32_t)r;
+        }
+    }
+}
+
+// Merge of the chunk partials of each heavy row, in chunk order (one
+// wavefront per row; each lane owns H*D/64 consecutive accumulator floats).
+template <typename T, int H, int D>
+__global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
+#pragma clang fp contract(off)
+    constexpr int HD = H * D;
+    constexpr int F = HD >= kWave ? HD / kWave : 1;
+    constexpr int EB = Elt<T>::kBytes;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int f0 = lane * F;
+    const int head = f0 / D;
+    const int32_t n_heavy = min(p.counters[CNT_HEAVY], p.cap_heavy);
+    const int nwaves = gridDim.x * kWavesPerBlock;
+    for (int hr = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; hr < n_heavy; hr += nwaves) {
+        if (f0 >= HD) continue;
+        const HeavyRow w = p.heavy[hr];
+        float m = -INFINITY, l = 0.0f, acc[F];
+#pragma unroll
+        for (int f = 0; f < F; ++f) acc[f] = 0.0f;
+        for (int c = 0; c < w.nch; ++c) {
+            const int64_t slot = w.base + c;
+            const float2 ml = p.part_ml[slot * H + head];
+            const float* a = p.part_acc + slot * HD + f0;
+            const float mn = fmaxf(m, ml.x);
+            const float ca = (m == mn) ? 1.0f : fast_exp2(m - mn);
+            const float cb = (ml.x == mn) ? 1.0f : fast_exp2(ml.x - mn);
+            l = l * ca + ml.y * cb;
+#pragma unroll
+            for (int f = 0; f < F; ++f) acc[f] = acc[f] * ca + a[f] * cb;
+            m = mn;
+        }
+        const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+        char* orow = p.out + (int64_t)w.row * HD * EB;
+#pragma unroll
+        for (int f = 0; f < F; ++f) {
+            const float o = acc[f] * inv;
+            if constexpr (EB == 4)
+                reinterpret_cast<float*>(orow)[f0 + f] = o;
+            else
+                reinterpret_cast<uint16_t*>(orow)[f0 + f] = (uint16_t)bf16_rne(o);
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) gt_csr_check_kernel(const int64_t* rowptr, const int32_t* colidx,
+                                                            int64_t N, int64_t E, int32_t* bad) {
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    const int64_t tid = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (tid == 0 && (rowptr[0] != 0 || rowptr[N] != E)) atomicOr(bad, 1);
+    for (int64_t i = tid; i < N; i += stride)
+        if (rowptr[i + 1] < rowptr[i]) atomicOr(bad, 1);
+    for (int64_t k = tid; k < E; k += stride)
+        if (colidx[k] < 0 || colidx[k] >= N) atomicOr(bad, 1);
+}
+
+// ----------------------------------------------------------------- host side
+
+thread_local std::string t_last_error;
+
+gt_status fail(gt_status s, const std::string& msg) {
+    t_last_error = msg;
+    return s;
+}
+
+gt_status hip_fail(hipError_t e, const char* what) {
+    return fail(GT_ERROR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+struct Profiler {
+    std::mutex mu;
+    bool on = false;
+    std::vector<std::array<hipEvent_t, 4>> pending;
+};
+Profiler& profiler() {
+    static Profiler* p = new Profiler();
+    return *p;
+}
+
+struct Args {
+    const int64_t* rowptr;
+    const int32_t* colidx;
+    const void* Q;
+    const void* K;
+    const void* V;
+    void* out;
+    int64_t N, E;
+    int32_t H, D;
+    float scale;
+};
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int device_cus(int dev) {
+    static int cache[64] = {0};
+    if (dev < 0 || dev >= 64) return 256;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+template <typename T, int H, int D>
+int attn_blocks_per_cu(int dev) {
+    static int cache[64] = {0};
+    if (dev < 0 || dev >= 64) return 4;
+    if (cache[dev] == 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, gt_attn_kernel<T, H, D>, kBlock, 0) != hipSuccess || nb <= 0)
+            nb = 4;
+        cache[dev] = nb;
+    }
+    return cache[dev];
+}
+
+template <typename T, int H, int D>
+gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
+    using Gm = Geo<T, H, D>;
+    int light_max = 4 * Gm::kU;
+    int heavy_min = 1024;
+    int chunk = 512;
+    int grid = 0;
+    if (tu) {
+        if (tu->light_max_deg > 0) light_max = tu->light_max_deg;
+        if (tu->heavy_min_deg > 0) heavy_min = tu->heavy_min_deg;
+        if (tu->chunk_edges > 0) chunk = (tu->chunk_edges + kWave - 1) / kWave * kWave;
+        if (tu->grid_blocks > 0) grid = tu->grid_blocks;
+    }
+    if (heavy_min <= light_max) heavy_min = light_max + 1;
+
+    int dev = 0;
+    hipError_t he = hipGetDevice(&dev);
+    if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+    if (grid <= 0) {
+        grid = device_cus(dev) * attn_blocks_per_cu<T, H, D>(dev);
+        const int64_t need = ((a.N + Gm::kP - 1) / Gm::kP + kWavesPerBlock - 1) / kWavesPerBlock;
+        if (need < grid) grid = (int)need;
+    }
+    grid = (grid + kXcds - 1) / kXcds * kXcds;
+
+    // workspace: counters | medium rows | heavy rows | chunk items | partial (m,l) | partial acc
+    const int64_t cap_heavy = a.E / heavy_min + 1;
+    const int64_t cap_chunks = a.E / chunk + cap_heavy + 1;
+    size_t off = 0;
+    const size_t o_cnt = off;      off = align_up(off + CNT_WORDS * sizeof(int32_t), 256);
+    const size_t o_med = off;      off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
+    const size_t o_heavy = off;    off = align_up(off + (size_t)cap_heavy * sizeof(HeavyRow), 256);
+    const size_t o_chunks = off;   off = align_up(off + (size_t)cap_chunks * sizeof(ChunkItem), 256);
+    const size_t o_ml = off;       off = align_up(off + (size_t)cap_chunks * H * sizeof(float2), 256);
+    const size_t o_acc = off;      off = align_up(off + (size_t)cap_chunks * H * D * sizeof(float), 256);
+    const size_t ws_bytes = off;
+
+    char* ws = nullptr;
+    he = hipMallocAsync(reinterpret_cast<void**>(&ws), ws_bytes, stream);
+    if (he != hipSuccess || !ws) {
+        (void)hipGetLastError();
+        return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(ws_bytes) + " bytes failed");
+    }
+
+    // After allocation every error path releases the workspace (stream-ordered).
+    auto bail = [&](gt_status st) {
+        (void)hipFreeAsync(ws, stream);
+        return st;
+    };
+
+    Profiler& pr = profiler();
+    bool prof;
+    {
+        std::lock_guard<std::mutex> lk(pr.mu);
+        prof = pr.on;
+    }
+    std::array<hipEvent_t, 4> ev{};
+    if (prof) {
+        for (auto& e : ev)
+            if ((he = hipEventCreate(&e)) != hipSuccess) return bail(hip_fail(he, "hipEventCreate"));
+        (void)hipEventRecord(ev[0], stream);
+    }
+
+    int32_t* counters = reinterpret_cast<int32_t*>(ws + o_cnt);
+    he = hipMemsetAsync(counters, 0, CNT_WORDS * sizeof(int32_t), stream);
+    if (he != hipSuccess) return bail(hip_fail(he, "hipMemsetAsync"));
+
+    PartParams pp;
+    pp.rowptr = a.rowptr;
+    pp.N = a.N;
+    pp.light_max = light_max;
+    pp.heavy_min = heavy_min;
+    pp.chunk = chunk;
+    pp.cap_heavy = (int32_t)cap_heavy;
+    pp.cap_chunks = (int32_t)cap_chunks;
+    pp.counters = counters;
+    pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
+    pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
+    pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
+    const int part_grid = (int)((a.N + kPartRowsPerBlock - 1) / kPartRowsPerBlock);
+    hipLaunchKernelGGL(gt_partition_kernel, dim3(part_grid), dim3(kBlock), 0, stream, pp);
+    if ((he = hipGetLastError()) != hipSuccess) return bail(hip_fail(he, "partition launch"));
+    if (prof) (void)hipEventRecord(ev[1], stream);
+
+    AttnParams ap;
+    ap.rowptr = a.rowptr;
+    ap.colidx = a.colidx;
+    ap.Q = static_cast<const char*>(a.Q);
+    ap.K = static_cast<const char*>(a.K);
+    ap.V = static_cast<const char*>(a.V);
+    ap.out = static_cast<char*>(a.out);
+    ap.N = a.N;
+    ap.c = a.scale * 1.4426950408889634f;
+    ap.light_max = light_max;
+    ap.cap_chunks = (int32_t)cap_chunks;
+    ap.counters = counters;
+    ap.med_list = pp.med_list;
+    ap.chunks = pp.chunks;
+    ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
+    ap.part_ml = reinterpret_cast<float2*>(ws + o_ml);
+    hipLaunchKernelGGL((gt_attn_kernel<T, H, D>), dim3(grid), dim3(kBlock), 0, stream, ap);
+    if ((he = hipGetLastError()) != hipSuccess) return bail(hip_fail(he, "attention launch"));
+    if (prof) (void)hipEventRecord(ev[2], stream);
+
+    MergeParams mp;
+    mp.cap_heavy = (int32_t)cap_heavy;
+    mp.counters = counters;
+    mp.heavy = pp.heavy;
+    mp.part_acc = ap.part_acc;
+    mp.part_ml = ap.part_ml;
+    mp.out = ap.out;
+    int merge_grid = (int)((cap_heavy + kWavesPerBlock - 1) / kWavesPerBlock);
+    const int merge_cap = device_cus(dev) * 8;
+    if (merge_grid > merge_cap) merge_grid = merge_cap;
+    if (merge_grid < 1) merge_grid = 1;
+    hipLaunchKernelGGL((gt_merge_kernel<T, H, D>), dim3(merge_grid), dim3(kBlock), 0, stream, mp);
+    if ((he = hipGetLastError()) != hipSuccess) return bail(hip_fail(he, "merge launch"));
+    if (prof) {
+        (void)hipEventRecord(ev[3], stream);
+        std::lock_guard<std::mutex> lk(pr.mu);
+        pr.pending.push_back(ev);
+    }
+
+    he = hipFreeAsync(ws, stream);
+    if (he != hipSuccess) return hip_fail(he, "hipFreeAsync");
+    return GT_SUCCESS;
+}
+
+using LaunchFn = gt_status (*)(const Args&, const gt_tuning*, hipStream_t);
+
+template <typename T>
+LaunchFn pick_hd(int32_t H, int32_t D) {
+#define GT_CASE(h, d) \
+    if (H == h && D == d) return &launch<T, h, d>;
+    GT_CASE(1, 32) GT_CASE(1, 64) GT_CASE(1, 128)
+    GT_CASE(2, 32) GT_CASE(2, 64) GT_CASE(2, 128)
+    GT_CASE(4, 32) GT_CASE(4, 64) GT_CASE(4, 128)
+    GT_CASE(8, 32) GT_CASE(8, 64) GT_CASE(8, 128)
+#undef GT_CASE
+    return nullptr;
+}
+
+bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + bn && y < x + an;
+}
+
+gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t stream) {
+    t_last_error.clear();
+    if (dtype != GT_DTYPE_F32 && dtype != GT_DTYPE_BF16) return fail(GT_ERROR_NOT_SUPPORTED, "unknown dtype");
+    if (a.N < 0 || a.N >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "N must be in [0, 2^31)");
+    if (a.E < 0 || a.E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
+    if (a.H < 1 || a.D < 1) return fail(GT_ERROR_INVALID_VALUE, "H and D must be positive");
+    if (!std::isfinite(a.scale)) return fail(GT_ERROR_INVALID_VALUE, "scale must be finite");
+    LaunchFn fn = dtype == GT_DTYPE_F32 ? pick_hd<float>(a.H, a.D) : pick_hd<bf16_tag>(a.H, a.D);
+    if (!fn)
+        return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +
+                                                std::to_string(a.D) + "); H in {1,2,4,8}, D in {32,64,128}");
+    if (a.N == 0) return GT_SUCCESS;
+    if (!a.rowptr) return fail(GT_ERROR_INVALID_VALUE, "rowptr is null");
+    if (a.E > 0 && !a.colidx) return fail(GT_ERROR_INVALID_VALUE, "colidx is null");
+    if (!a.Q || !a.K || !a.V || !a.out) return fail(GT_ERROR_INVALID_VALUE, "Q, K, V and out must be non-null");
+    for (const void* ptr : {a.Q, a.K, a.V, static_cast<const void*>(a.out)})
+        if (reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
+            return fail(GT_ERROR_INVALID_VALUE, "Q, K, V and out must be 16-byte aligned");
+    const size_t bytes = (size_t)a.N * a.H * a.D * (dtype == GT_DTYPE_F32 ? 4 : 2);
+    for (const void* in : {a.Q, a.K, a.V})
+        if (overlaps(a.out, bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "out overlaps Q, K or V");
+    return fn(a, tu, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+gt_status gt_attn_fwd(const int64_t* rowptr, const int32_t* colidx, const float* Q, const float* K,
+                      const float* V, float* out, int64_t N, int64_t E, int32_t H, int32_t D, float scale,
+                      hipStream_t stream) {
+    return run(GT_DTYPE_F32, Args{rowptr, colidx, Q, K, V, out, N, E, H, D, scale}, nullptr, stream);
+}
+
+gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const uint16_t* Q, const uint16_t* K,
+                           const uint16_t* V, uint16_t* out, int64_t N, int64_t E, int32_t H, int32_t D,
+                           float scale, hipStream_t stream) {
+    return run(GT_DTYPE_BF16, Args{rowptr, colidx, Q, K, V, out, N, E, H, D, scale}, nullptr, stream);
+}
+
+gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const void* Q,
+                         const void* K, const void* V, void* out, int64_t N, int64_t E, int32_t H, int32_t D,
+                         float scale, const gt_tuning* tuning, hipStream_t stream) {
+    return run(dtype, Args{rowptr, colidx, Q, K, V, out, N, E, H, D, scale}, tuning, stream);
+}
+
+gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t N, int64_t E, int32_t* valid,
+                          hipStream_t stream) {
+    t_last_error.clear();
+    if (!valid) return fail(GT_ERROR_INVALID_VALUE, "valid is null");
+    *valid = 0;
+    if (N < 0 || E < 0 || E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "bad N or E");
+    if (!rowptr || (E > 0 && !colidx)) return fail(GT_ERROR_INVALID_VALUE, "null CSR pointer");
+    int32_t* bad = nullptr;
+    hipError_t he = hipMallocAsync(reinterpret_cast<void**>(&bad), sizeof(int32_t), stream);
+    if (he != hipSuccess) return fail(GT_ERROR_OUT_OF_MEMORY, "flag allocation failed");
+    if ((he = hipMemsetAsync(bad, 0, sizeof(int32_t), stream)) != hipSuccess) return hip_fail(he, "hipMemsetAsync");
+    const int64_t work = N > E ? N : E;
+    int grid = (int)((work + kBlock - 1) / kBlock);
+    if (grid > 4096) grid = 4096;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(gt_csr_check_kernel, dim3(grid), dim3(kBlock), 0, stream, rowptr, colidx, N, E, bad);
+    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "validate launch");
+    int32_t h_bad = 1;
+    if ((he = hipMemcpyAsync(&h_bad, bad, sizeof(int32_t), hipMemcpyDeviceToHost, stream)) != hipSuccess)
+        return hip_fail(he, "hipMemcpyAsync");
+    (void)hipFreeAsync(bad, stream);
+    if ((he = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(he, "hipStreamSynchronize");
+    *valid = h_bad == 0 ? 1 : 0;
+    return GT_SUCCESS;
+}
+
+const char* gt_status_string(gt_status s) {
+    switch (s) {
+        case GT_SUCCESS: return "success";
+        case GT_ERROR_INVALID_VALUE: return "invalid value";
+        case GT_ERROR_NOT_SUPPORTED: return "not supported";
+        case GT_ERROR_OUT_OF_MEMORY: return "out of memory";
+        case GT_ERROR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* gt_last_error_message(void) { return t_last_error.c_str(); }
+
+gt_status gt_profile_enable(int32_t enable) {
+    Profiler& pr = profiler();
+    std::lock_guard<std::mutex> lk(pr.mu);
+    for (auto& ev : pr.pending) {
+        (void)hipEventSynchronize(ev[3]);
+        for (auto e : ev) (void)hipEventDestroy(e);
+    }
+    pr.pending.clear();
+    pr.on = enable != 0;
+    return GT_SUCCESS;
+}
+
+gt_status gt_profile_collect(double ms[3], int64_t* calls) {
+    t_last_error.clear();
+    if (!ms || !calls) return fail(GT_ERROR_INVALID_VALUE, "null output");
+    Profiler& pr = profiler();
+    std::lock_guard<std::mutex> lk(pr.mu);
+    ms[0] = ms[1] = ms[2] = 0.0;
+    *calls = 0;
+    gt_status st = GT_SUCCESS;
+    for (auto& ev : pr.pending) {
+        hipError_t he = hipEventSynchronize(ev[3]);
+        if (he != hipSuccess) {
+            st = hip_fail(he, "hipEventSynchronize");
+        } else {
+            for (int k = 0; k < 3; ++k) {
+                float t = 0.0f;
+                if (hipEventElapsedTime(&t, ev[k], ev[k + 1]) == hipSuccess) ms[k] += t;
+            }
+            ++*calls;
+        }
+        for (auto e : ev) (void)hipEventDestroy(e);
+    }
+    pr.pending.clear();
+    return st;
+}
+
+}  // extern "C"

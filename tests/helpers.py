@@ -86,3 +86,49 @@ def load_worked_example(name: str = "worked_example.txt") -> dict:
     rows["ABS"] = arr(ABS, lambda s: float(Fraction(s)), np.float64)
     rows["LSE"] = arr(LSE, lnconv, np.float64)
     return rows
+
+
+# ------------------------------------------------------------ device helpers
+
+def to_device(a):
+    """numpy -> torch CUDA tensor; uint16 arrays (bf16 bits) become torch.bfloat16."""
+    import torch
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_host_f32(t) -> np.ndarray:
+    """torch CUDA tensor -> float32 numpy (bf16 widened exactly)."""
+    import torch
+    if t.dtype == torch.bfloat16:
+        return bf16_bits_to_f32(t.view(torch.int16).cpu().numpy().view(np.uint16))
+    return t.cpu().numpy()
+
+
+def run_gpu(rowptr, colidx, Q, K, V, scale, tuning=None, stream=None):
+    """One call of the HIP path through the C ABI; returns float32 host output."""
+    import torch
+    import paper_2605_31500_amd as gt
+    dt = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    out = torch.empty_like(dt[2])
+    gt.gt_attn_fwd_ex(*dt, out, scale, tuning=tuning, stream=stream)
+    torch.cuda.synchronize()
+    return to_host_f32(out)
+
+
+def sample_rows(rowptr: np.ndarray, n_random: int, n_top: int, seed: int = 0) -> np.ndarray:
+    """Rows to check at full size: the n_top highest-degree rows, n_random rows
+    drawn uniformly (seeded), the first and last rows, and one row of each
+    degree 0, 1 and 2 when present."""
+    import synth
+    N = rowptr.size - 1
+    deg = np.diff(rowptr)
+    top = np.argsort(deg, kind="stable")[-n_top:]
+    rnd = np.floor(synth.uniform01(seed, synth.STREAM_EXTRA + 7, n_random) * N).astype(np.int64)
+    extra = [0, N - 1]
+    for d in (0, 1, 2):
+        hit = np.flatnonzero(deg == d)
+        if hit.size:
+            extra.append(int(hit[0]))
+    return np.unique(np.concatenate([top, rnd, np.array(extra, dtype=np.int64)]))

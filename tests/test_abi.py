@@ -1,0 +1,86 @@
+"""C-ABI library checks that need no GPU: the library loads, exports every
+function include/gt_attn.h declares, and rejects bad arguments on the host
+before any device work (every call here fails validation, so no pointer is
+ever dereferenced and no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gt_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gt_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2605_31500_amd as gt
+    return gt.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    import paper_2605_31500_amd as gt
+    names = declared_functions()
+    assert set(names) == set(gt.EXPORTED_SYMBOLS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code in range(5):
+        assert lib.gt_status_string(code)
+    assert lib.gt_status_string(99) == b"unknown status"
+
+
+FAKE = 0x10000  # never dereferenced: each call below fails validation first
+
+
+def call(lib, dtype=0, rowptr=FAKE, colidx=FAKE, Q=FAKE, K=FAKE + 0x100000, V=FAKE + 0x200000,
+         out=FAKE + 0x300000, N=10, E=20, H=4, D=32, scale=0.1):
+    P = ctypes.c_void_p
+    return lib.gt_attn_fwd_ex(dtype, P(rowptr), P(colidx), P(Q), P(K), P(V), P(out), N, E, H, D,
+                              ctypes.c_float(scale), None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=3), 2), (dict(D=48), 2), (dict(D=256), 2), (dict(dtype=7), 2),
+    (dict(N=-1), 1), (dict(E=-5), 1), (dict(E=1 << 31), 1), (dict(N=1 << 31), 1),
+    (dict(H=0), 1), (dict(scale=float("inf")), 1), (dict(scale=float("nan")), 1),
+    (dict(rowptr=0), 1), (dict(colidx=0), 1), (dict(Q=0), 1), (dict(out=0), 1),
+    (dict(K=FAKE + 8), 1),                      # misaligned
+    (dict(out=FAKE + 0x200000 + 1024), 1),      # out overlaps V
+    (dict(out=FAKE), 1),                        # out aliases Q
+])
+def test_host_validation(lib, kw, status):
+    assert call(lib, **kw) == status
+    assert lib.gt_last_error_message()
+
+
+def test_empty_graph_is_a_no_op(lib):
+    # N == 0 enqueues nothing and touches no pointer
+    assert call(lib, N=0, E=0, rowptr=FAKE) == 0
+    assert lib.gt_last_error_message() == b""
+
+
+def test_profile_without_calls(lib):
+    assert lib.gt_profile_enable(1) == 0
+    ms = (ctypes.c_double * 3)()
+    calls = ctypes.c_int64(-1)
+    assert lib.gt_profile_collect(ms, ctypes.byref(calls)) == 0
+    assert calls.value == 0 and list(ms) == [0.0, 0.0, 0.0]
+    assert lib.gt_profile_enable(0) == 0
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    import paper_2605_31500_amd as gt
+    z = torch.zeros(3, 1, 32)
+    with pytest.raises(ValueError):
+        gt.gt_attn_fwd(torch.zeros(4, dtype=torch.int64), torch.zeros(0, dtype=torch.int32), z, z,
+                       z, z, 0.1)

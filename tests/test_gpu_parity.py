@@ -1,0 +1,78 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+the same seeded inputs.  Gate: max_e |x - r| / max(|r|, absagg) <= 1e-5 for
+fp32 features and <= 2e-2 for bf16 features (fp32 accumulation, bf16 output)."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, load_worked_example,
+                           run_gpu, sample_rows)
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(h, d) for h in (1, 2, 4, 8) for d in (32, 64, 128)]
+FORCED_SPLIT = {"light_max_deg": 2, "heavy_min_deg": 6, "chunk_edges": 64, "grid_blocks": 0}
+
+
+def tol(dtype):
+    return TOL_F32 if dtype == "f32" else TOL_BF16
+
+
+def check(w_or_arrays, dtype, tuning=None, rows=None):
+    rowptr, colidx, Q, K, V, scale = w_or_arrays
+    got = run_gpu(rowptr, colidx, Q, K, V, scale, tuning=tuning)
+    ref, absagg, _ = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, rows=rows, want_lse=False)
+    if rows is not None:
+        got = got[rows]
+    err = gate_error(got, ref, absagg)
+    assert np.all(np.isfinite(got))
+    assert err <= tol(dtype), "gate error %.3g > %.3g" % (err, tol(dtype))
+    return err, got, ref
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_worked_example(dtype):
+    ex = load_worked_example()
+    # zero-pad the head dimension 2 -> 32 (a compiled shape): dots are unchanged
+    # and the padded output columns must come out as exactly 0
+    pad = lambda x: np.ascontiguousarray(np.pad(x, ((0, 0), (0, 0), (0, 30))))
+    Q, K, V = (pad(ex[k]) for k in ("Q", "K", "V"))
+    if dtype == "bf16":  # small integers: exact in bf16
+        Q, K, V = ((x.view(np.uint32) >> 16).astype(np.uint16) for x in (Q, K, V))
+    got = run_gpu(ex["rowptr"], ex["colidx"], Q, K, V, ex["scale"])
+    # fp32 evaluation: ~1e-7; bf16 output adds its round-to-nearest step,
+    # at most half an ulp = 2^-8 relative
+    bound = 1e-6 if dtype == "f32" else 2.0 ** -8 + 1e-6
+    assert gate_error(got[:, :, :2], ex["OUT"], ex["ABS"]) <= bound
+    assert np.all(got[:, :, 2:] == 0)
+    assert np.array_equal(got[1, :, :2], ex["V"][1])  # single-entry row is exact
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("H,D", SHAPES)
+def test_ragged_small(H, D, dtype, split):
+    N = 300
+    rowptr, colidx = synth.ragged_graph(H * 1000 + D, N, max_deg=24, empty_frac=0.1,
+                                        hubs={7: 299, 100: 150, 299: 70}, self_loops=True,
+                                        dup_frac=0.05, shuffle=True)
+    Q, K, V = synth.features(H * 1000 + D, N, H, D, dtype)
+    check((rowptr, colidx, Q, K, V, np.float32(1 / math.sqrt(D))), dtype,
+          tuning=FORCED_SPLIT if split else None)
+
+
+@pytest.mark.parametrize("idx", [0, 1])
+def test_full_config_all_rows(idx):
+    w = synth.config(idx)
+    check((w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale), w.dtype)
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4])
+def test_full_config_sampled_rows(idx):
+    w = synth.config(idx)
+    print("config", idx, w.name, "N", w.N, "E", w.E, flush=True)
+    rows = sample_rows(w.rowptr, n_random=3000, n_top=64)
+    check((w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale), w.dtype, rows=rows)
