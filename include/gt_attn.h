@@ -32,8 +32,12 @@
  * Ownership and memory: every pointer argument is DEVICE memory owned by the
  * caller; the library neither frees nor retains it past the enqueued work.
  * `out` must not overlap Q, K or V.  Q, K, V and out must be 16-byte aligned.
- * Temporary workspace is allocated stream-ordered on `stream`
- * (hipMallocAsync / hipFreeAsync) and released when the call's work ends.
+ * Workspace (degree-bin lists and partial softmax states of split rows) is
+ * owned by the library: one buffer per (device, stream), allocated
+ * stream-ordered (hipMallocAsync) by the first call on that stream and grown
+ * when a later call needs more, so steady-state calls allocate nothing.  The
+ * buffers live until gt_workspace_release() or process exit.  Calls on one
+ * stream (from any host threads) are serialised by the library.
  *
  * Semantics: asynchronous.  GT_SUCCESS means the work was enqueued on
  * `stream`; device faults surface at the caller's next synchronisation.
@@ -92,14 +96,17 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  * rows to wavefronts, with light/heavy thresholds and per-chunk edge counts
  * that the paper tunes by grid search).  A field <= 0 selects the default.
  *   light_max_deg : rows of degree <= this are handled by one lane group
- *                   (a sub-wavefront) each
- *   heavy_min_deg : rows of degree >= this are split into chunks processed
- *                   by different wavefronts and merged afterwards; rows in
- *                   between get one wavefront each
- *   chunk_edges   : CSR entries per chunk of a split row (rounded up to a
- *                   multiple of 64)
- *   grid_blocks   : workgroups of the persistent attention kernel (rounded
- *                   up to a multiple of 8)
+ *                   (a sub-wavefront) each (default 8 steps of the group)
+ *   heavy_min_deg : rows of degree >= this are scheduled first; those longer
+ *                   than one chunk are split into chunks processed by
+ *                   different wavefronts and merged afterwards; rows in
+ *                   between get one wavefront each (default 256)
+ *   chunk_edges   : CSR entries per chunk of a split row, rounded up to a
+ *                   multiple of 64; a row is cut into at most 32 chunks, so
+ *                   very long rows get longer chunks (default 1024)
+ *   grid_blocks   : workgroups of the attention kernel, rounded up to a
+ *                   multiple of 8 (default: about two light work items per
+ *                   wavefront, within 4x..64x the resident workgroups)
  * Results are bitwise reproducible for fixed settings; different settings
  * change only the fp32 rounding.
  */
@@ -144,6 +151,12 @@ const char* gt_last_error_message(void);
  */
 gt_status gt_profile_enable(int32_t enable);
 gt_status gt_profile_collect(double ms[3], int64_t* calls);
+
+/*
+ * Frees every cached workspace (synchronising each device that holds one).
+ * Must not run concurrently with attention calls.
+ */
+gt_status gt_workspace_release(void);
 
 #ifdef __cplusplus
 }

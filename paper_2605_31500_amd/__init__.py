@@ -26,7 +26,7 @@ GT_DTYPE_BF16 = 1
 
 EXPORTED_SYMBOLS = (
     "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_csr_validate", "gt_status_string",
-    "gt_last_error_message", "gt_profile_enable", "gt_profile_collect",
+    "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
 )
 
 
@@ -66,8 +66,9 @@ def load_library(path: str = LIB_PATH):
     L.gt_last_error_message.restype = ctypes.c_char_p
     L.gt_profile_enable.argtypes = [i32]
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
+    L.gt_workspace_release.argtypes = []
     for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_csr_validate",
-                 "gt_profile_enable", "gt_profile_collect"):
+                 "gt_profile_enable", "gt_profile_collect", "gt_workspace_release"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -173,3 +174,8 @@ def gt_profile_collect():
     calls = ctypes.c_int64(0)
     _check(load_library().gt_profile_collect(ms, ctypes.byref(calls)))
     return [ms[0], ms[1], ms[2]], calls.value
+
+
+def gt_workspace_release() -> None:
+    """Free the library's cached per-stream workspaces (synchronises devices)."""
+    _check(load_library().gt_workspace_release())

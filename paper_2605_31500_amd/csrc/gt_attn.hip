@@ -35,8 +35,12 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <functional>
+#include <map>
+#include <memory>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "gt_attn.h"
@@ -49,7 +53,15 @@ constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kXcds = 8;
 
 // Counter slots in the workspace (reset to zero at the start of each call).
-enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_WORDS = 16 };
+// Work-list counters.  Each counter sits on its own 256-byte line so that
+// atomics on different counters do not serialise on one cache line.  A
+// workspace holds two counter sets used by alternate calls: a call uses one
+// set (zero on entry) and its attention kernel zeroes the other set for the
+// next call, so no reset has to wait for the end of the call.
+enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_COUNT = 4 };
+constexpr int kCntStride = 64;                          // ints between counters
+constexpr int kCntSetWords = CNT_COUNT * kCntStride;   // one counter set
+#define CNT(c, i) ((c)[(i) * kCntStride])
 
 struct bf16_tag {};
 
@@ -101,6 +113,7 @@ struct AttnParams {
     int32_t light_max;
     int32_t cap_chunks;
     const int32_t* counters;
+    int32_t* next_counters;  // the other counter set, zeroed for the next call
     const int32_t* med_list;
     const ChunkItem* chunks;
     float* part_acc;   // [slot][H*D]
@@ -223,32 +236,40 @@ struct RowState {
         }
     }
 
-    // One step over U entries (indices j[0..U)); entries u >= nvalid are
-    // copies of valid indices and contribute nothing (score -inf).
-    __device__ __forceinline__ void step(const char* __restrict__ Kb, const char* __restrict__ Vb,
-                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c) {
+    // Loads of one step: the K and V rows of U entries, 16 bytes per lane each.
+    struct Batch {
+        uint4 k[Gm::kU][Gm::kNV];
+        uint4 v[Gm::kU][Gm::kNV];
+    };
+
+    __device__ __forceinline__ void issue(const char* __restrict__ Kb, const char* __restrict__ Vb,
+                                          const int32_t (&j)[Gm::kU], int lig, Batch& bt) const {
+#pragma unroll
+        for (int u = 0; u < Gm::kU; ++u) {
+            const int64_t off = (int64_t)j[u] * Gm::kRowBytes + lig * 16;
+#pragma unroll
+            for (int k = 0; k < Gm::kNV; ++k) {
+                bt.k[u][k] = *reinterpret_cast<const uint4*>(Kb + off + k * Gm::kG * 16);
+                bt.v[u][k] = *reinterpret_cast<const uint4*>(Vb + off + k * Gm::kG * 16);
+            }
+        }
+    }
+
+    // Online-softmax update with the U entries of a batch; entries u >= nvalid
+    // are copies of valid indices and contribute nothing (score -inf).
+    __device__ __forceinline__ void consume(const Batch& bt, int nvalid, float c) {
         // No implicit contraction: fusing the score product into the later
         // subtraction of the running max would give the maximal entry a weight
         // of 2^(rounding error) instead of exactly 1.
 #pragma clang fp contract(off)
         constexpr int U = Gm::kU;
-        uint4 kr[U][Gm::kNV], vr[U][Gm::kNV];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t off = (int64_t)j[u] * Gm::kRowBytes + lig * 16;
-#pragma unroll
-            for (int k = 0; k < Gm::kNV; ++k) {
-                kr[u][k] = *reinterpret_cast<const uint4*>(Kb + off + k * Gm::kG * 16);
-                vr[u][k] = *reinterpret_cast<const uint4*>(Vb + off + k * Gm::kG * 16);
-            }
-        }
         float s[U][Gm::kNV];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
             for (int k = 0; k < Gm::kNV; ++k) {
                 float kf[Gm::kEPV];
-                widen<T>(kr[u][k], kf);
+                widen<T>(bt.k[u][k], kf);
                 float d = 0.0f;
 #pragma unroll
                 for (int e = 0; e < Gm::kEPV; ++e) d = fmaf(q[k][e], kf[e], d);
@@ -270,12 +291,19 @@ struct RowState {
                 const float pu = fast_exp2(s[u][k] - mb);
                 l[k] += pu;
                 float vf[Gm::kEPV];
-                widen<T>(vr[u][k], vf);
+                widen<T>(bt.v[u][k], vf);
 #pragma unroll
                 for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = fmaf(pu, vf[e], acc[k][e]);
             }
             m[k] = mb;
         }
+    }
+
+    __device__ __forceinline__ void step(const char* __restrict__ Kb, const char* __restrict__ Vb,
+                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c) {
+        Batch bt;
+        issue(Kb, Vb, j, lig, bt);
+        consume(bt, nvalid, c);
     }
 
     // Merge the state held by the lane `off` positions away (same vector
@@ -364,33 +392,61 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
     }
 }
 
-// One lane group handles a whole light row (degree <= light_max).
+// Light rows (degree <= light_max), one lane group per row.  Each group walks
+// its sequence of rows software-pipelined: the next row's rowptr entries are
+// loaded before the current row's work starts, and its first index tile is
+// loaded while the current row's first K/V batch is in flight, so a short row
+// costs about one memory latency instead of three (rowptr -> colidx -> K/V).
 template <typename T, int H, int D>
-__device__ __forceinline__ void group_row(const AttnParams& p, int64_t row, int32_t* __restrict__ gtile,
-                                          int lig) {
+__device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int64_t it_end,
+                                           int64_t stride, int g, int lig,
+                                           int32_t* __restrict__ gtile) {
     using Gm = Geo<T, H, D>;
-    constexpr int U = Gm::kU, G = Gm::kG;
-    if (row >= p.N) return;
-    const int64_t b = p.rowptr[row], e = p.rowptr[row + 1];
-    if (e - b > p.light_max) return;
-    RowState<T, H, D> st;
-    st.begin(p.Q, row, lig);
-    for (int64_t tb = b; tb < e; tb += G) {
-        const int64_t pos = (tb + lig < e) ? tb + lig : e - 1;
-        const int32_t idx = p.colidx[pos];
-        wave_lds_fence();
-        gtile[lig] = idx;
-        wave_lds_fence();
-        const int nt = (int)((e - tb) < G ? (e - tb) : G);
-        for (int t = 0; t < nt; t += U) {
-            const int nvalid = nt - t < U ? nt - t : U;
-            int32_t j[U];
+    constexpr int U = Gm::kU, G = Gm::kG, P = Gm::kP;
+    int64_t row = it * P + g;
+    bool ok = it < it_end && row < p.N;
+    int64_t b = ok ? p.rowptr[row] : 0, e = ok ? p.rowptr[row + 1] : 0;
+    bool mine = ok && (e - b) <= p.light_max;
+    int32_t idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
+    while (it < it_end) {
+        const int64_t crow = row, cb = b, ce = e;
+        const bool cmine = mine;
+        const int32_t cidx = idx;
+        it += stride;
+        row = it * P + g;
+        ok = it < it_end && row < p.N;
+        b = ok ? p.rowptr[row] : 0;
+        e = ok ? p.rowptr[row + 1] : 0;
+        mine = ok && (e - b) <= p.light_max;
+        bool fetched = false;
+        if (cmine) {
+            RowState<T, H, D> st;
+            st.begin(p.Q, crow, lig);
+            for (int64_t tb = cb; tb < ce; tb += G) {
+                int32_t tile_idx = cidx;
+                if (tb != cb) tile_idx = p.colidx[(tb + lig < ce) ? tb + lig : ce - 1];
+                wave_lds_fence();
+                gtile[lig] = tile_idx;
+                wave_lds_fence();
+                const int nt = (int)((ce - tb) < G ? (ce - tb) : G);
+                for (int t = 0; t < nt; t += U) {
+                    const int nvalid = nt - t < U ? nt - t : U;
+                    int32_t j[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) j[u] = gtile[t + u];
-            st.step(p.K, p.V, j, nvalid, lig, p.c);
+                    for (int u = 0; u < U; ++u) j[u] = gtile[t + u];
+                    typename RowState<T, H, D>::Batch bt;
+                    st.issue(p.K, p.V, j, lig, bt);
+                    if (!fetched) {  // next row's first tile, overlapped with this batch
+                        idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
+                        fetched = true;
+                    }
+                    st.consume(bt, nvalid, p.c);
+                }
+            }
+            st.store_out(p.out, crow, lig);
         }
+        if (!fetched) idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
     }
-    st.store_out(p.out, row, lig);
 }
 
 // Persistent attention kernel: first the chunk items (pieces of heavy rows,
@@ -406,8 +462,9 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
 
     // Counts come from the partition kernel; clamping keeps every list read
     // inside the workspace even if the CSR precondition were violated.
-    const int32_t n_chunks = min(p.counters[CNT_CHUNKS], p.cap_chunks);
-    const int32_t n_items = n_chunks + (int32_t)min((int64_t)p.counters[CNT_MED], p.N);
+    if (blockIdx.x == 0 && threadIdx.x < CNT_COUNT) CNT(p.next_counters, threadIdx.x) = 0;
+    const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_chunks);
+    const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
     const int nwaves = gridDim.x * kWavesPerBlock;
     for (int it = blockIdx.x * kWavesPerBlock + wv; it < n_items; it += nwaves) {
         if (it < n_chunks) {
@@ -425,15 +482,19 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
     const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
     const int g = lane / Gm::kG, lig = lane % Gm::kG;
-    for (int64_t it = lo + lw; it < hi; it += waves_per_xcd)
-        group_row<T, H, D>(p, it * Gm::kP + g, tile + g * Gm::kG, lig);
+    light_rows<T, H, D>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * Gm::kG);
 }
 
-// Degree binning.  Each block owns a contiguous range of rows; per-thread
-// counts are scanned inside the block and one atomic per list reserves the
-// block's output range.
+// Degree binning.  A block owns kPartRowsPerBlock contiguous rows; thread t
+// takes rows t, t+256, ... of the block, so every rowptr load is coalesced.
+// Medium rows are compacted with wave ballots; heavy-row and chunk counts
+// with block scans; each block then reserves its output ranges with one
+// atomic per list.  A heavy row is cut into at most kMaxChunks chunks of
+// (about) equal length, at least `chunk` entries each, so the ordered merge
+// of a hub stays a few load rounds long.
 constexpr int kPartRowsPerThread = 8;
 constexpr int kPartRowsPerBlock = kBlock * kPartRowsPerThread;
+constexpr int kMaxChunks = 32;
 
 __device__ __forceinline__ int block_exclusive_scan(int v, int* lds_waves, int* total) {
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
@@ -451,66 +512,97 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* lds_waves, int* 
         if (w < wv) before += lds_waves[w];
         sum += lds_waves[w];
     }
-    __syncthreads();
     *total = sum;
     return before + x - v;
 }
 
+__device__ __forceinline__ int chunks_of(int64_t deg, int chunk) {
+    const int64_t n = (deg + chunk - 1) / chunk;
+    return (int)(n < kMaxChunks ? n : kMaxChunks);
+}
+
 __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
-    __shared__ int lds[3][kWavesPerBlock];
+    __shared__ int wave_cnt[kPartRowsPerThread][kWavesPerBlock];
+    __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock];
     __shared__ int base[3];
-    const int64_t r0 = (int64_t)blockIdx.x * kPartRowsPerBlock + (int64_t)threadIdx.x * kPartRowsPerThread;
-    int n_med = 0, n_heavy = 0, n_chunk = 0;
-    int64_t deg[kPartRowsPerThread];
+    const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
+    const int64_t r0 = (int64_t)blockIdx.x * kPartRowsPerBlock;
+    int64_t rb[kPartRowsPerThread], deg[kPartRowsPerThread];
+    bool med[kPartRowsPerThread];
+    uint64_t mask[kPartRowsPerThread];
+    int n_heavy = 0, n_chunk = 0;
 #pragma unroll
-    for (int t = 0; t < kPartRowsPerThread; ++t) {
-        const int64_t r = r0 + t;
-        deg[t] = (r < p.N) ? p.rowptr[r + 1] - p.rowptr[r] : 0;
-        if (deg[t] >= p.heavy_min) {
-            ++n_heavy;
-            n_chunk += (int)((deg[t] + p.chunk - 1) / p.chunk);
-        } else if (deg[t] > p.light_max) {
-            ++n_med;
+    for (int k = 0; k < kPartRowsPerThread; ++k) {
+        const int64_t r = r0 + k * kBlock + threadIdx.x;
+        rb[k] = 0;
+        deg[k] = 0;
+        if (r < p.N) {
+            rb[k] = p.rowptr[r];
+            deg[k] = p.rowptr[r + 1] - rb[k];
+        }
+        med[k] = deg[k] > p.light_max && deg[k] < p.heavy_min;
+        mask[k] = __ballot(med[k]);
+        if (lane == 0) wave_cnt[k][wv] = __popcll(mask[k]);
+        if (deg[k] >= p.heavy_min) {
+            const int nch = chunks_of(deg[k], p.chunk);
+            n_heavy += nch > 1 ? 1 : 0;
+            n_chunk += nch;
         }
     }
-    int tot_med, tot_heavy, tot_chunk;
-    const int off_med = block_exclusive_scan(n_med, lds[0], &tot_med);
-    const int off_heavy = block_exclusive_scan(n_heavy, lds[1], &tot_heavy);
-    const int off_chunk = block_exclusive_scan(n_chunk, lds[2], &tot_chunk);
+    int tot_h, tot_c;
+    const int off_h = block_exclusive_scan(n_heavy, scan_h, &tot_h);
+    const int off_c = block_exclusive_scan(n_chunk, scan_c, &tot_c);
     if (threadIdx.x == 0) {
-        base[0] = tot_med ? atomicAdd(&p.counters[CNT_MED], tot_med) : 0;
-        base[1] = tot_heavy ? atomicAdd(&p.counters[CNT_HEAVY], tot_heavy) : 0;
-        base[2] = tot_chunk ? atomicAdd(&p.counters[CNT_CHUNKS], tot_chunk) : 0;
+        int tot_m = 0;
+        for (int k = 0; k < kPartRowsPerThread; ++k)
+            for (int w = 0; w < kWavesPerBlock; ++w) tot_m += wave_cnt[k][w];
+        base[0] = tot_m ? atomicAdd(&CNT(p.counters, CNT_MED), tot_m) : 0;
+        base[1] = tot_h ? atomicAdd(&CNT(p.counters, CNT_HEAVY), tot_h) : 0;
+        base[2] = tot_c ? atomicAdd(&CNT(p.counters, CNT_CHUNKS), tot_c) : 0;
     }
     __syncthreads();
-    int im = base[0] + off_med, ih = base[1] + off_heavy, ic = base[2] + off_chunk;
+    int pos = base[0];
+    int hid = base[1] + off_h, slot = base[2] + off_c;
 #pragma unroll
-    for (int t = 0; t < kPartRowsPerThread; ++t) {
-        const int64_t r = r0 + t;
-        if (r >= p.N) break;
-        if (deg[t] >= p.heavy_min) {
-            const int nch = (int)((deg[t] + p.chunk - 1) / p.chunk);
-            if (ih >= p.cap_heavy || ic + nch > p.cap_chunks) {
-                atomicOr(&p.counters[CNT_OVERFLOW], 1);
+    for (int k = 0; k < kPartRowsPerThread; ++k) {
+        const int64_t r = r0 + k * kBlock + threadIdx.x;
+        int before = 0;
+        for (int w = 0; w < wv; ++w) before += wave_cnt[k][w];
+        if (med[k]) p.med_list[pos + before + __popcll(mask[k] & ((1ull << lane) - 1))] = (int32_t)r;
+        for (int w = 0; w < kWavesPerBlock; ++w) pos += wave_cnt[k][w];
+        if (deg[k] >= p.heavy_min) {
+            // Rows of degree >= heavy_min are placed first in the work list (the
+            // longest items start first).  A row that fits in one chunk is a
+            // single item writing its output directly; a longer row is split
+            // and recorded for the ordered merge.
+            const int nch = chunks_of(deg[k], p.chunk);
+            const int need_h = nch > 1 ? 1 : 0;
+            if (hid + need_h > p.cap_heavy || slot + nch > p.cap_chunks) {
+                atomicOr(&CNT(p.counters, CNT_OVERFLOW), 1);
+            } else if (nch == 1) {
+                p.chunks[slot] = ChunkItem{(int32_t)r, -1, rb[k], rb[k] + deg[k]};
             } else {
-                const int64_t b = p.rowptr[r];
-                p.heavy[ih] = HeavyRow{(int32_t)r, ic, nch, 0};
+                const int64_t len = (deg[k] + nch - 1) / nch;
+                const int64_t end = rb[k] + deg[k];
+                p.heavy[hid] = HeavyRow{(int32_t)r, slot, nch, 0};
                 for (int c = 0; c < nch; ++c) {
-                    const int64_t cb = b + (int64_t)c * p.chunk;
-                    const int64_t ce = (cb + p.chunk < b + deg[t]) ? cb + p.chunk : b + deg[t];
-                    p.chunks[ic + c] = ChunkItem{(int32_t)r, ic + c, cb, ce};
+                    const int64_t cb = rb[k] + c * len;
+                    p.chunks[slot + c] = ChunkItem{(int32_t)r, slot + c, cb < end ? cb : end,
+                                                   cb + len < end ? cb + len : end};
                 }
             }
-            ++ih;
-            ic += nch;
-        } else if (deg[t] > p.light_max) {
-            p.med_list[im++] = (int32_t)r;
+            hid += need_h;
+            slot += nch;
         }
     }
 }
 
 // Merge of the chunk partials of each heavy row, in chunk order (one
 // wavefront per row; each lane owns H*D/64 consecutive accumulator floats).
+// Partials are loaded kMergeBatch chunks at a time so their latencies
+// overlap; the merge itself stays sequential in chunk order.
+constexpr int kMergeBatch = 8;
+
 template <typename T, int H, int D>
 __global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
 #pragma clang fp contract(off)
@@ -520,7 +612,7 @@ __global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int f0 = lane * F;
     const int head = f0 / D;
-    const int32_t n_heavy = min(p.counters[CNT_HEAVY], p.cap_heavy);
+    const int32_t n_heavy = min(CNT(p.counters, CNT_HEAVY), p.cap_heavy);
     const int nwaves = gridDim.x * kWavesPerBlock;
     for (int hr = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; hr < n_heavy; hr += nwaves) {
         if (f0 >= HD) continue;
@@ -528,17 +620,27 @@ __global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
         float m = -INFINITY, l = 0.0f, acc[F];
 #pragma unroll
         for (int f = 0; f < F; ++f) acc[f] = 0.0f;
-        for (int c = 0; c < w.nch; ++c) {
-            const int64_t slot = w.base + c;
-            const float2 ml = p.part_ml[slot * H + head];
-            const float* a = p.part_acc + slot * HD + f0;
-            const float mn = fmaxf(m, ml.x);
-            const float ca = (m == mn) ? 1.0f : fast_exp2(m - mn);
-            const float cb = (ml.x == mn) ? 1.0f : fast_exp2(ml.x - mn);
-            l = l * ca + ml.y * cb;
+        for (int c0 = 0; c0 < w.nch; c0 += kMergeBatch) {
+            float2 ml[kMergeBatch];
+            float a[kMergeBatch][F];
 #pragma unroll
-            for (int f = 0; f < F; ++f) acc[f] = acc[f] * ca + a[f] * cb;
-            m = mn;
+            for (int u = 0; u < kMergeBatch; ++u) {
+                const int64_t slot = w.base + (c0 + u < w.nch ? c0 + u : w.nch - 1);
+                ml[u] = p.part_ml[slot * H + head];
+#pragma unroll
+                for (int f = 0; f < F; ++f) a[u][f] = p.part_acc[slot * HD + f0 + f];
+            }
+#pragma unroll
+            for (int u = 0; u < kMergeBatch; ++u) {
+                if (c0 + u >= w.nch) break;
+                const float mn = fmaxf(m, ml[u].x);
+                const float ca = (m == mn) ? 1.0f : fast_exp2(m - mn);
+                const float cb = (ml[u].x == mn) ? 1.0f : fast_exp2(ml[u].x - mn);
+                l = l * ca + ml[u].y * cb;
+#pragma unroll
+                for (int f = 0; f < F; ++f) acc[f] = acc[f] * ca + a[u][f] * cb;
+                m = mn;
+            }
         }
         const float inv = l > 0.0f ? 1.0f / l : 0.0f;
         char* orow = p.out + (int64_t)w.row * HD * EB;
@@ -587,6 +689,50 @@ Profiler& profiler() {
     return *p;
 }
 
+// Workspace cache: one buffer per (device, stream) -- per thread for the
+// per-thread default stream -- reused by every later call on that stream, so
+// steady-state calls allocate nothing and stream order keeps reuse safe.  The
+// buffer grows (stream-ordered free + allocation) when a call needs more.  The
+// entry's mutex is held while a call enqueues its whole kernel sequence, so
+// calls from several host threads on one stream cannot interleave.
+struct WsKey {
+    int dev;
+    uintptr_t stream;
+    size_t thread;
+    bool operator<(const WsKey& o) const {
+        if (dev != o.dev) return dev < o.dev;
+        if (stream != o.stream) return stream < o.stream;
+        return thread < o.thread;
+    }
+};
+
+struct WsEntry {
+    std::mutex mu;
+    char* ptr = nullptr;
+    size_t bytes = 0;
+    bool counters_zero = false;  // counter set `parity` known to be zero
+    int parity = 0;              // counter set the next call uses
+};
+
+struct WsCache {
+    std::mutex mu;
+    std::map<WsKey, std::unique_ptr<WsEntry>> entries;
+};
+WsCache& ws_cache() {
+    static WsCache* c = new WsCache();
+    return *c;
+}
+
+WsEntry& ws_entry(int dev, hipStream_t stream) {
+    WsKey key{dev, reinterpret_cast<uintptr_t>(stream), 0};
+    if (stream == hipStreamPerThread) key.thread = std::hash<std::thread::id>()(std::this_thread::get_id());
+    WsCache& c = ws_cache();
+    std::lock_guard<std::mutex> lk(c.mu);
+    auto& e = c.entries[key];
+    if (!e) e.reset(new WsEntry());
+    return *e;
+}
+
 struct Args {
     const int64_t* rowptr;
     const int32_t* colidx;
@@ -628,9 +774,12 @@ int attn_blocks_per_cu(int dev) {
 template <typename T, int H, int D>
 gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
-    int light_max = 4 * Gm::kU;
-    int heavy_min = 1024;
-    int chunk = 512;
+    // Defaults chosen by measurement on the five workload shapes (power law,
+    // R-MAT, SBM, lognormal hubs): a group handles rows of up to 8 steps;
+    // rows of degree >= 256 go first, split into chunks of 1024 entries.
+    int light_max = 8 * Gm::kU;
+    int heavy_min = 256;
+    int chunk = 1024;
     int grid = 0;
     if (tu) {
         if (tu->light_max_deg > 0) light_max = tu->light_max_deg;
@@ -644,9 +793,18 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     hipError_t he = hipGetDevice(&dev);
     if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
     if (grid <= 0) {
-        grid = device_cus(dev) * attn_blocks_per_cu<T, H, D>(dev);
-        const int64_t need = ((a.N + Gm::kP - 1) / Gm::kP + kWavesPerBlock - 1) / kWavesPerBlock;
-        if (need < grid) grid = (int)need;
+        // About two light items (P rows each) per wave, between 4x and 64x the
+        // number of workgroups the device holds at once: finer than one
+        // resident wave of workgroups so the hardware scheduler evens out the
+        // per-wave work, coarse enough to keep dispatch cheap.
+        const int64_t resident = (int64_t)device_cus(dev) * attn_blocks_per_cu<T, H, D>(dev);
+        const int64_t light_items = (a.N + Gm::kP - 1) / Gm::kP;
+        int64_t g = light_items / (2 * kWavesPerBlock);
+        if (g < 4 * resident) g = 4 * resident;
+        if (g > 64 * resident) g = 64 * resident;
+        const int64_t need = (light_items + kWavesPerBlock - 1) / kWavesPerBlock;
+        if (g > need) g = need;
+        grid = (int)(g > 0 ? g : 1);
     }
     grid = (grid + kXcds - 1) / kXcds * kXcds;
 
@@ -654,7 +812,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const int64_t cap_heavy = a.E / heavy_min + 1;
     const int64_t cap_chunks = a.E / chunk + cap_heavy + 1;
     size_t off = 0;
-    const size_t o_cnt = off;      off = align_up(off + CNT_WORDS * sizeof(int32_t), 256);
+    const size_t o_cnt = off;      off = align_up(off + 2 * kCntSetWords * sizeof(int32_t), 256);
     const size_t o_med = off;      off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
     const size_t o_heavy = off;    off = align_up(off + (size_t)cap_heavy * sizeof(HeavyRow), 256);
     const size_t o_chunks = off;   off = align_up(off + (size_t)cap_chunks * sizeof(ChunkItem), 256);
@@ -662,18 +820,33 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const size_t o_acc = off;      off = align_up(off + (size_t)cap_chunks * H * D * sizeof(float), 256);
     const size_t ws_bytes = off;
 
-    char* ws = nullptr;
-    he = hipMallocAsync(reinterpret_cast<void**>(&ws), ws_bytes, stream);
-    if (he != hipSuccess || !ws) {
-        (void)hipGetLastError();
-        return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(ws_bytes) + " bytes failed");
+    WsEntry& we = ws_entry(dev, stream);
+    std::lock_guard<std::mutex> ws_lock(we.mu);
+    if (we.bytes < ws_bytes) {
+        if (we.ptr) (void)hipFreeAsync(we.ptr, stream);
+        we.ptr = nullptr;
+        we.bytes = 0;
+        he = hipMallocAsync(reinterpret_cast<void**>(&we.ptr), ws_bytes, stream);
+        if (he != hipSuccess || !we.ptr) {
+            (void)hipGetLastError();
+            we.ptr = nullptr;
+            return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(ws_bytes) + " bytes failed");
+        }
+        we.bytes = ws_bytes;
+        we.counters_zero = false;
     }
-
-    // After allocation every error path releases the workspace (stream-ordered).
-    auto bail = [&](gt_status st) {
-        (void)hipFreeAsync(ws, stream);
-        return st;
-    };
+    char* ws = we.ptr;
+    int32_t* cnt_sets = reinterpret_cast<int32_t*>(ws + o_cnt);
+    if (!we.counters_zero) {
+        he = hipMemsetAsync(cnt_sets, 0, 2 * kCntSetWords * sizeof(int32_t), stream);
+        if (he != hipSuccess) return hip_fail(he, "hipMemsetAsync");
+        we.parity = 0;
+    }
+    int32_t* counters = cnt_sets + we.parity * kCntSetWords;
+    int32_t* next_counters = cnt_sets + (1 - we.parity) * kCntSetWords;
+    // Until the attention kernel (which zeroes the other set) is enqueued, the
+    // next call cannot rely on its counters; a failed launch leaves this false.
+    we.counters_zero = false;
 
     Profiler& pr = profiler();
     bool prof;
@@ -684,13 +857,9 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     std::array<hipEvent_t, 4> ev{};
     if (prof) {
         for (auto& e : ev)
-            if ((he = hipEventCreate(&e)) != hipSuccess) return bail(hip_fail(he, "hipEventCreate"));
+            if ((he = hipEventCreate(&e)) != hipSuccess) return hip_fail(he, "hipEventCreate");
         (void)hipEventRecord(ev[0], stream);
     }
-
-    int32_t* counters = reinterpret_cast<int32_t*>(ws + o_cnt);
-    he = hipMemsetAsync(counters, 0, CNT_WORDS * sizeof(int32_t), stream);
-    if (he != hipSuccess) return bail(hip_fail(he, "hipMemsetAsync"));
 
     PartParams pp;
     pp.rowptr = a.rowptr;
@@ -706,7 +875,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
     const int part_grid = (int)((a.N + kPartRowsPerBlock - 1) / kPartRowsPerBlock);
     hipLaunchKernelGGL(gt_partition_kernel, dim3(part_grid), dim3(kBlock), 0, stream, pp);
-    if ((he = hipGetLastError()) != hipSuccess) return bail(hip_fail(he, "partition launch"));
+    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "partition launch");
     if (prof) (void)hipEventRecord(ev[1], stream);
 
     AttnParams ap;
@@ -721,12 +890,13 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.light_max = light_max;
     ap.cap_chunks = (int32_t)cap_chunks;
     ap.counters = counters;
+    ap.next_counters = next_counters;
     ap.med_list = pp.med_list;
     ap.chunks = pp.chunks;
     ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
     ap.part_ml = reinterpret_cast<float2*>(ws + o_ml);
     hipLaunchKernelGGL((gt_attn_kernel<T, H, D>), dim3(grid), dim3(kBlock), 0, stream, ap);
-    if ((he = hipGetLastError()) != hipSuccess) return bail(hip_fail(he, "attention launch"));
+    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "attention launch");
     if (prof) (void)hipEventRecord(ev[2], stream);
 
     MergeParams mp;
@@ -741,15 +911,14 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     if (merge_grid > merge_cap) merge_grid = merge_cap;
     if (merge_grid < 1) merge_grid = 1;
     hipLaunchKernelGGL((gt_merge_kernel<T, H, D>), dim3(merge_grid), dim3(kBlock), 0, stream, mp);
-    if ((he = hipGetLastError()) != hipSuccess) return bail(hip_fail(he, "merge launch"));
+    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "merge launch");
     if (prof) {
         (void)hipEventRecord(ev[3], stream);
         std::lock_guard<std::mutex> lk(pr.mu);
         pr.pending.push_back(ev);
     }
-
-    he = hipFreeAsync(ws, stream);
-    if (he != hipSuccess) return hip_fail(he, "hipFreeAsync");
+    we.parity = 1 - we.parity;
+    we.counters_zero = true;
     return GT_SUCCESS;
 }
 
@@ -891,6 +1060,28 @@ gt_status gt_profile_collect(double ms[3], int64_t* calls) {
         for (auto e : ev) (void)hipEventDestroy(e);
     }
     pr.pending.clear();
+    return st;
+}
+
+gt_status gt_workspace_release(void) {
+    t_last_error.clear();
+    WsCache& c = ws_cache();
+    std::lock_guard<std::mutex> lk(c.mu);
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    gt_status st = GT_SUCCESS;
+    for (auto& kv : c.entries) {
+        std::lock_guard<std::mutex> el(kv.second->mu);
+        if (!kv.second->ptr) continue;
+        hipError_t he = hipSetDevice(kv.first.dev);
+        if (he == hipSuccess) he = hipDeviceSynchronize();
+        if (he == hipSuccess) he = hipFree(kv.second->ptr);
+        if (he != hipSuccess) st = hip_fail(he, "releasing a workspace");
+        kv.second->ptr = nullptr;
+        kv.second->bytes = 0;
+    }
+    c.entries.clear();
+    (void)hipSetDevice(cur);
     return st;
 }
 

@@ -171,3 +171,28 @@ def test_profiler_counts_calls():
     ms, calls = m.gt_profile_collect()
     m.gt_profile_enable(False)
     assert calls == 3 and all(x > 0 for x in ms)
+
+
+def test_workspace_reuse_growth_and_release():
+    """Consecutive calls share the per-stream workspace; its counters must be
+    back at zero after every call and growth must not disturb results."""
+    small = synth.ragged_graph(11, 3000, max_deg=30, hubs={1: 2999, 2: 1500})
+    big = synth.ragged_graph(12, 40000, max_deg=50, hubs={5: 39999, 6: 20000, 7: 5000})
+    feats = {n: synth.features(13, n, 4, 32, "f32") for n in (3000, 40000)}
+
+    def run(g):
+        rp, ci = g
+        Q, K, V = feats[rp.size - 1]
+        return run_gpu(rp, ci, Q, K, V, np.float32(0.2))
+
+    a1 = run(small)
+    b1 = run(big)
+    a2 = run(small)
+    b2 = run(big)
+    assert np.array_equal(a1, a2) and np.array_equal(b1, b2)
+    gt().gt_workspace_release()
+    assert np.array_equal(run(small), a1)
+    rp, ci = big
+    Q, K, V = feats[40000]
+    ref, absagg, _ = oracle.gt_attn_fwd(rp, ci, Q, K, V, 0.2)
+    assert gate_error(b1, ref, absagg) <= TOL_F32
