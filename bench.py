@@ -95,6 +95,9 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=1, help="workload index 0..4 (default 1)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
+                    help="enable the matrix-core path for dense 64-id windows holding at "
+                         "least MIN in-window entries (bf16, H*D <= 128)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run plain device-to-device copies of MIB "
                          "MiB (reference kernel for scaling HBM byte counters)")
@@ -120,8 +123,10 @@ def main() -> int:
     out = torch.empty_like(dev[2])
     stream = torch.cuda.current_stream()
 
+    tuning = {"dense_tiles": args.dense_tiles} if args.dense_tiles else None
+
     def step():
-        gt.gt_attn_fwd_ex(*dev, out, w.scale, stream=stream)
+        gt.gt_attn_fwd_ex(*dev, out, w.scale, tuning=tuning, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -164,7 +169,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": w.describe(),
+        "config": dict(w.describe(), **({"dense_tiles": args.dense_tiles} if args.dense_tiles else {})),
         "roofline": {
             "bound": "hbm",
             "kernel": "gt_attn_kernel",

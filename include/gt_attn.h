@@ -107,14 +107,26 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  *   grid_blocks   : workgroups of the attention kernel, rounded up to a
  *                   multiple of 8 (default: about two light work items per
  *                   wavefront, within 4x..64x the resident workgroups)
+ *   dense_tiles   : 0 (default) = off.  A positive value enables the matrix-
+ *                   core path for locally dense graphs (Section 3.3 and
+ *                   Appendix D.3: block-sparse tiles): rows are grouped in
+ *                   aligned windows of 64 ids; a window whose light rows hold
+ *                   at least `dense_tiles` entries pointing inside the window
+ *                   computes those entries as masked 64x64 tiles with bf16
+ *                   MFMA (scores and P*V), then streams each row's remaining
+ *                   entries.  bf16 features with H*D <= 128 only; ignored
+ *                   otherwise.  Softmax weights inside tiles are rounded to
+ *                   bf16 before the P*V product (the normaliser uses the same
+ *                   rounded weights).  256 suits 50%-dense 64-blocks.
  * Results are bitwise reproducible for fixed settings; different settings
- * change only the fp32 rounding.
+ * change only the rounding.
  */
 typedef struct gt_tuning {
     int32_t light_max_deg;
     int32_t heavy_min_deg;
     int32_t chunk_edges;
     int32_t grid_blocks;
+    int32_t dense_tiles;
 } gt_tuning;
 
 /*

@@ -37,6 +37,7 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <type_traits>
 #include <memory>
 #include <mutex>
 #include <string>
@@ -118,6 +119,7 @@ struct AttnParams {
     const ChunkItem* chunks;
     float* part_acc;   // [slot][H*D]
     float2* part_ml;   // [slot][H]: (running max in log2 units, sum)
+    int32_t skip_light;  // light rows are handled by the dense-tile kernel
 };
 
 struct PartParams {
@@ -449,7 +451,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
     }
 }
 
-// Persistent attention kernel: first the chunk items (pieces of heavy rows,
+// Attention kernel: first the chunk items (pieces of heavy rows,
 // then whole medium rows), one wavefront each; then the light rows, P per
 // wavefront, in XCD-contiguous ranges.
 template <typename T, int H, int D>
@@ -482,7 +484,329 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
     const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
     const int g = lane / Gm::kG, lig = lane % Gm::kG;
-    light_rows<T, H, D>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * Gm::kG);
+    if (!p.skip_light) light_rows<T, H, D>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * Gm::kG);
+}
+
+// ------------------------------------------------------- dense-tile path
+//
+// Locally dense windows (Section 3.3 and Appendix D.3 of the paper pack local
+// neighbourhoods into tiles for matrix cores; this is a gfx950 design of the
+// same idea, not the paper's 16x8 TCB format).  Rows are grouped in aligned
+// windows of 64; the window's own 64 ids are its tile columns.  In tile mode
+// this kernel handles every light row (one workgroup per window):
+//   1. stage the window's rowptr, the CSR entries of its light rows, its K
+//      rows and its V rows (transposed) in LDS with independent loads;
+//   2. per light row, a 64-bit mask of its in-window entries (a row with a
+//      repeated in-window entry cannot be a mask and does not use the tile);
+//   3. if the window holds at least `min_entries` masked entries, per head and
+//      per 16-row strip (one wave each):
+//        S^T = K_w Q_strip^T  (bf16 MFMA 16x16x32, fp32 accumulate),
+//      masked row-wise softmax statistics, and acc = P V_w (second MFMA, P
+//      rounded to bf16; the normaliser sums the same rounded weights);
+//   4. every light row then streams its remaining entries (all of them for a
+//      row without a tile) with the CSR online-softmax step, continuing from
+//      the tile's (m, l, acc), and writes its output.
+// Non-light rows are left to the wave items of the CSR kernel.
+//
+// MFMA operand layout of v_mfma_f32_16x16x32_bf16 (64 lanes, l = lane):
+//   A (16x32): lane l holds A[l%16][8*(l/16) + j], j = 0..7
+//   B (32x16): lane l holds B[8*(l/16) + j][l%16]
+//   C (16x16): lane l holds C[4*(l/16) + i][l%16], i = 0..3
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kWin = 64;          // window rows = tile columns
+constexpr int kWinMaxDeg = 64;    // light rows handled here have at most this degree
+constexpr int kVtStride = 72;     // padded row of the transposed V tile (bf16 elements)
+
+struct TileParams {
+    const int64_t* rowptr;
+    const int32_t* colidx;
+    const char* Q;
+    const char* K;
+    const char* V;
+    char* out;
+    int64_t N;
+    float c;  // scale * log2(e)
+    int32_t light_max;  // <= kWinMaxDeg
+    int32_t min_entries;
+};
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+template <int H, int D>
+struct TileLds {
+    static constexpr int HD = H * D;
+    static constexpr int KST = HD + 8;  // padded K row (bf16 elements)
+    int64_t rp[kWin + 1];
+    int32_t lpre[kWin + 1];              // prefix of light-row degrees
+    int32_t ebeg[kWin], eend[kWin];      // each row's entries within idx
+    int32_t idx[kWin * kWinMaxDeg];      // the window's entries (see staging)
+    uint64_t masks[kWin];
+    int32_t wave_cnt[kWavesPerBlock];
+    union alignas(16) {
+        struct {
+            uint16_t k[kWin][KST];
+            uint16_t vt[HD][kVtStride];
+        } kv;
+        float acc[kWavesPerBlock][16][HD];
+    } big;
+    float2 ml[kWavesPerBlock][16][H];
+    int32_t ctile[kWavesPerBlock][kWave / (H * D / 8) * kWinMaxDeg];  // per lane group: one row's entries
+};
+
+template <int H, int D>
+__global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
+    using Gm = Geo<bf16_tag, H, D>;
+    using L = TileLds<H, D>;
+    constexpr int HD = H * D;
+    constexpr int G = Gm::kG, P = Gm::kP, U = Gm::kU;
+    static_assert(HD <= 128 && D % 32 == 0, "tile path shapes");
+    __shared__ __attribute__((aligned(16))) L lds;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+    const int g16 = lane >> 4, n16 = lane & 15;  // MFMA lane coordinates
+    const int64_t r0 = (int64_t)blockIdx.x * kWin;
+    const int64_t wend = r0 + kWin;
+
+    // ---- 1. staging
+    if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
+    for (int v = tid; v < kWin * (HD / 8); v += kBlock) {
+        const int cc = v / (HD / 8), e0 = (v % (HD / 8)) * 8;
+        uint4 kx = make_uint4(0, 0, 0, 0), vx = make_uint4(0, 0, 0, 0);
+        if (r0 + cc < p.N) {
+            kx = *reinterpret_cast<const uint4*>(p.K + ((r0 + cc) * HD + e0) * 2);
+            vx = *reinterpret_cast<const uint4*>(p.V + ((r0 + cc) * HD + e0) * 2);
+        }
+        *reinterpret_cast<uint4*>(&lds.big.kv.k[cc][e0]) = kx;
+        const uint32_t w4[4] = {vx.x, vx.y, vx.z, vx.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            lds.big.kv.vt[e0 + 2 * q][cc] = (uint16_t)(w4[q] & 0xFFFFu);
+            lds.big.kv.vt[e0 + 2 * q + 1][cc] = (uint16_t)(w4[q] >> 16);
+        }
+    }
+    // this lane's strip row of Q (all heads), as MFMA B operands
+    const int64_t qrow = r0 + 16 * wv + n16;
+    uint4 qreg[HD / 32];
+#pragma unroll
+    for (int t = 0; t < HD / 32; ++t) {
+        qreg[t] = make_uint4(0, 0, 0, 0);
+        if (qrow < p.N) qreg[t] = *reinterpret_cast<const uint4*>(p.Q + (qrow * HD + 32 * t + 8 * g16) * 2);
+    }
+    __syncthreads();
+    // Entries: if the window's whole CSR range fits, it is copied as is (one
+    // coalesced pass); otherwise only the light rows' entries are packed.
+    const int64_t n_all = lds.rp[kWin] - lds.rp[0];
+    const bool contiguous = n_all <= kWin * kWinMaxDeg;
+    if (wv == 0) {
+        const int64_t deg = lds.rp[lane + 1] - lds.rp[lane];
+        int x = (deg <= p.light_max) ? (int)deg : 0;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int y = __shfl_up(x, o);
+            if (lane >= o) x += y;
+        }
+        lds.lpre[lane + 1] = x;
+        if (lane == 0) lds.lpre[0] = 0;
+        if (contiguous) {
+            lds.ebeg[lane] = (int32_t)(lds.rp[lane] - lds.rp[0]);
+            lds.eend[lane] = (int32_t)(lds.rp[lane + 1] - lds.rp[0]);
+        } else {
+            lds.eend[lane] = x;
+            lds.ebeg[lane] = (deg <= p.light_max) ? x - (int)deg : x;
+        }
+    }
+    __syncthreads();
+    {
+        constexpr int kPer = kWin * kWinMaxDeg / kBlock;  // entries per thread
+        const int n_ent = contiguous ? (int)n_all : lds.lpre[kWin];
+        int32_t vals[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int f = tid + k * kBlock;
+            int64_t src = lds.rp[0] + f;
+            if (!contiguous && f < n_ent) {
+                int lo = 0, hi = kWin;  // owner row: the last row with lpre[row] <= f
+                while (hi - lo > 1) {
+                    const int mid = (lo + hi) >> 1;
+                    if (lds.lpre[mid] <= f) lo = mid; else hi = mid;
+                }
+                src = lds.rp[lo] + (f - lds.lpre[lo]);
+            }
+            vals[k] = f < n_ent ? p.colidx[src] : 0;
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+            if (tid + k * kBlock < n_ent) lds.idx[tid + k * kBlock] = vals[k];
+    }
+    __syncthreads();
+
+    // ---- 2. in-window masks: 4 lanes per row, 16 rows per wave
+    const int srow = lane >> 2, sub = lane & 3;
+    const int wrow = 16 * wv + srow;  // row within the window
+    const int64_t r = r0 + wrow;
+    const bool light = r < p.N && (lds.rp[wrow + 1] - lds.rp[wrow]) <= p.light_max;
+    const int lb = lds.ebeg[wrow], le = light ? lds.eend[wrow] : lds.ebeg[wrow];
+    uint64_t mk = 0;
+    int cnt = 0;
+    for (int t = lb + sub; t < le; t += 4) {
+        const int64_t j = lds.idx[t];
+        if (j >= r0 && j < wend) {
+            mk |= 1ull << (j - r0);
+            ++cnt;
+        }
+    }
+    mk |= shfl_xor_u64(mk, 1);
+    mk |= shfl_xor_u64(mk, 2);
+    cnt += __shfl_xor(cnt, 1);
+    cnt += __shfl_xor(cnt, 2);
+    const bool tile_ok = light && __popcll(mk) == cnt;  // no repeated in-window entry
+    if (sub == 0) lds.masks[wrow] = tile_ok ? mk : 0;
+    int wc = (sub == 0 && tile_ok) ? cnt : 0;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) wc += __shfl_xor(wc, o);
+    if (lane == 0) lds.wave_cnt[wv] = wc;
+    const uint64_t ok_bits = __ballot(sub == 0 && tile_ok);     // bit 4*sr: strip row sr
+    const uint64_t light_bits = __ballot(sub == 0 && light);
+    __syncthreads();
+    int total = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) total += lds.wave_cnt[w];
+    const bool dense = total >= p.min_entries;  // uniform over the workgroup
+
+    // ---- 3. tiles
+    float mx[H], lsum[H];
+    f32x4_t oacc[H][D / 16];
+    if (dense) {
+        const uint64_t rmask = lds.masks[16 * wv + n16];
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+            f32x4_t sacc[4];
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) sacc[mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks) {
+                const bf16x8_t bq = __builtin_bit_cast(bf16x8_t, qreg[(h * D) / 32 + ks]);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    const bf16x8_t ak = __builtin_bit_cast(
+                        bf16x8_t, *reinterpret_cast<const uint4*>(&lds.big.kv.k[16 * mt + n16][h * D + 32 * ks + 8 * g16]));
+                    sacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, bq, sacc[mt], 0, 0, 0);
+                }
+            }
+            // lane holds S[strip row n16][window column 16*mt + 4*g16 + i] = sacc[mt][i]
+            float pr[16];
+            float m = -INFINITY;
+            {
+#pragma clang fp contract(off)
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int cc = 16 * mt + 4 * g16 + i;
+                        const float sv = ((rmask >> cc) & 1ull) ? sacc[mt][i] * p.c : -INFINITY;
+                        pr[4 * mt + i] = sv;
+                        m = fmaxf(m, sv);
+                    }
+                m = fmaxf(m, __shfl_xor(m, 16));
+                m = fmaxf(m, __shfl_xor(m, 32));
+            }
+            uint32_t pb[16];
+            float ls = 0.0f;
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                const float pv = (m == -INFINITY) ? 0.0f : fast_exp2(pr[t] - m);
+                pb[t] = bf16_rne(pv);
+                ls += __uint_as_float(pb[t] << 16);
+            }
+            ls += __shfl_xor(ls, 16);
+            ls += __shfl_xor(ls, 32);
+            mx[h] = m;
+            lsum[h] = ls;
+            // acc = P V_w; K order of step ks, slot 8*g16 + j: window column
+            // 16*(2ks + j/4) + 4*g16 + j%4, i.e. exactly the weights this lane holds
+#pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt) oacc[h][dt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const uint4 au = make_uint4(pb[8 * ks + 0] | (pb[8 * ks + 1] << 16), pb[8 * ks + 2] | (pb[8 * ks + 3] << 16),
+                                            pb[8 * ks + 4] | (pb[8 * ks + 5] << 16), pb[8 * ks + 6] | (pb[8 * ks + 7] << 16));
+                const bf16x8_t ap = __builtin_bit_cast(bf16x8_t, au);
+#pragma unroll
+                for (int dt = 0; dt < D / 16; ++dt) {
+                    const int e = h * D + 16 * dt + n16;
+                    const uint2 lo = *reinterpret_cast<const uint2*>(&lds.big.kv.vt[e][32 * ks + 4 * g16]);
+                    const uint2 hi = *reinterpret_cast<const uint2*>(&lds.big.kv.vt[e][32 * ks + 16 + 4 * g16]);
+                    const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+                    oacc[h][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bv, oacc[h][dt], 0, 0, 0);
+                }
+            }
+        }
+    }
+    __syncthreads();  // K / V tiles no longer read: their LDS now holds the strip results
+    if (dense) {
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+#pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) lds.big.acc[wv][4 * g16 + i][h * D + 16 * dt + n16] = oacc[h][dt][i];
+            if (g16 == 0) lds.ml[wv][n16][h] = make_float2(mx[h], lsum[h]);
+        }
+    }
+    wave_lds_fence();
+
+    // ---- 4. remaining entries of each light row, CSR online softmax, output
+    const int g = lane / G, lig = lane % G;
+    int32_t* gtile = lds.ctile[wv] + g * kWinMaxDeg;
+    for (int pass = 0; pass < 16 / P; ++pass) {
+        const int sr = pass * P + g;
+        if (!((light_bits >> (4 * sr)) & 1ull)) continue;
+        const bool use_tile = dense && ((ok_bits >> (4 * sr)) & 1ull);
+        const int wr = 16 * wv + sr;
+        const int64_t row = r0 + wr;
+        RowState<bf16_tag, H, D> st;
+        st.begin(p.Q, row, lig);
+        if (use_tile) {
+#pragma unroll
+            for (int k = 0; k < Gm::kNV; ++k) {
+                const int v = lig + k * G;
+                const float2 ml = lds.ml[wv][sr][v / Gm::kHL];
+                st.m[k] = ml.x;
+                st.l[k] = ml.y;
+#pragma unroll
+                for (int q = 0; q < Gm::kEPV; ++q) st.acc[k][q] = lds.big.acc[wv][sr][v * Gm::kEPV + q];
+            }
+        }
+        // gather the row's remaining entries (outside the tile) into gtile
+        const int eb = lds.ebeg[wr], ee = lds.eend[wr];
+        int n_take = 0;
+        for (int tb = eb; tb < ee; tb += G) {
+            const bool in = tb + lig < ee;
+            const int32_t idx = lds.idx[in ? tb + lig : ee - 1];
+            const bool take = in && !(use_tile && idx >= r0 && idx < wend);
+            const uint64_t bal = __ballot(take);
+            const uint32_t gbits = (uint32_t)((bal >> (g * G)) & ((1ull << G) - 1));
+            if (take) gtile[n_take + __popc(gbits & ((1u << lig) - 1u))] = idx;
+            n_take += __popc(gbits);
+        }
+        wave_lds_fence();
+        for (int t = 0; t < n_take; t += U) {
+            const int nvalid = n_take - t < U ? n_take - t : U;
+            int32_t j[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) j[u] = gtile[(t + u < n_take) ? t + u : n_take - 1];
+            st.step(p.K, p.V, j, nvalid, lig, p.c);
+        }
+        wave_lds_fence();
+        st.store_out(p.out, row, lig);
+    }
 }
 
 // Degree binning.  A block owns kPartRowsPerBlock contiguous rows; thread t
@@ -781,17 +1105,26 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     int heavy_min = 256;
     int chunk = 1024;
     int grid = 0;
+    int tile_min = 0;  // dense-tile windows off
     if (tu) {
+        if (tu->dense_tiles > 0) tile_min = tu->dense_tiles;
         if (tu->light_max_deg > 0) light_max = tu->light_max_deg;
         if (tu->heavy_min_deg > 0) heavy_min = tu->heavy_min_deg;
         if (tu->chunk_edges > 0) chunk = (tu->chunk_edges + kWave - 1) / kWave * kWave;
         if (tu->grid_blocks > 0) grid = tu->grid_blocks;
     }
     if (heavy_min <= light_max) heavy_min = light_max + 1;
+    constexpr bool kTileShape = std::is_same<T, bf16_tag>::value && H * D <= 128 && D % 32 == 0;
+    const bool tiles = kTileShape && tile_min > 0;
+    if (tiles && light_max > kWinMaxDeg) light_max = kWinMaxDeg;
 
     int dev = 0;
     hipError_t he = hipGetDevice(&dev);
     if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+    if (grid <= 0 && tiles) {
+        // light rows belong to the tile kernel: only the wave items remain
+        grid = 4 * device_cus(dev) * attn_blocks_per_cu<T, H, D>(dev);
+    }
     if (grid <= 0) {
         // About two light items (P rows each) per wave, between 4x and 64x the
         // number of workgroups the device holds at once: finer than one
@@ -876,6 +1209,24 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const int part_grid = (int)((a.N + kPartRowsPerBlock - 1) / kPartRowsPerBlock);
     hipLaunchKernelGGL(gt_partition_kernel, dim3(part_grid), dim3(kBlock), 0, stream, pp);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "partition launch");
+    if constexpr (kTileShape) {
+        if (tiles) {
+            TileParams tp;
+            tp.rowptr = a.rowptr;
+            tp.colidx = a.colidx;
+            tp.Q = static_cast<const char*>(a.Q);
+            tp.K = static_cast<const char*>(a.K);
+            tp.V = static_cast<const char*>(a.V);
+            tp.out = static_cast<char*>(a.out);
+            tp.N = a.N;
+            tp.c = a.scale * 1.4426950408889634f;
+            tp.light_max = light_max;
+            tp.min_entries = tile_min;
+            const int tgrid = (int)((a.N + kWin - 1) / kWin);
+            hipLaunchKernelGGL((gt_tile_kernel<H, D>), dim3(tgrid), dim3(kBlock), 0, stream, tp);
+            if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "tile launch");
+        }
+    }
     if (prof) (void)hipEventRecord(ev[1], stream);
 
     AttnParams ap;
@@ -895,6 +1246,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.chunks = pp.chunks;
     ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
     ap.part_ml = reinterpret_cast<float2*>(ws + o_ml);
+    ap.skip_light = tiles ? 1 : 0;
     hipLaunchKernelGGL((gt_attn_kernel<T, H, D>), dim3(grid), dim3(kBlock), 0, stream, ap);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "attention launch");
     if (prof) (void)hipEventRecord(ev[2], stream);

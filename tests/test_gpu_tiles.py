@@ -1,0 +1,108 @@
+"""GPU parity of the dense-tile (MFMA) path for locally dense windows.
+
+Graphs are 64-id block models with irregularities added so that every
+fallback runs: a partial last window, rows with a repeated in-window entry
+(left to the CSR kernel), a row long enough to be split (front path), empty
+rows, rows whose only entries lie outside their window, and windows below the
+density threshold."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.helpers import TOL_BF16, bf16_bits_to_f32, gate_error, run_gpu, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+TILE_SHAPES = [(1, 32), (1, 64), (1, 128), (2, 32), (2, 64), (4, 32)]
+
+
+def csr_from_rows(rows):
+    rowptr = np.zeros(len(rows) + 1, dtype=np.int64)
+    rowptr[1:] = np.cumsum([len(r) for r in rows])
+    colidx = np.concatenate([np.asarray(r, dtype=np.int32) for r in rows]) if rowptr[-1] else \
+        np.zeros(0, dtype=np.int32)
+    return rowptr, colidx
+
+
+def irregular_block_graph(seed, n_windows=12, tail=37):
+    N = 64 * n_windows + tail
+    rp, ci = synth.sbm_graph(seed, N, 64, 4)
+    rows = [list(ci[rp[i]:rp[i + 1]]) for i in range(N)]
+    u = synth.uniform01(seed, synth.STREAM_EXTRA + 3, 4 * N)
+    rows[3] = rows[3] + [rows[3][0]]                 # repeated in-window entry
+    rows[70] = rows[70] + [rows[70][1], rows[70][1]]  # repeated twice
+    rows[5] = []                                      # empty row in a dense window
+    rows[130] = [int(x) for x in np.floor(u[:300] * N)]  # long row, split into chunks
+    rows[200] = [(200 + 64 * 3) % N, (200 + 64 * 5) % N]  # only out-of-window entries
+    # window 9 made sparse (below any sensible threshold): keep only self-loops
+    for i in range(64 * 9, 64 * 10):
+        rows[i] = [i]
+    return csr_from_rows(rows)
+
+
+def check(rowptr, colidx, Q, K, V, scale, tiles, rows=None):
+    got = run_gpu(rowptr, colidx, Q, K, V, scale, tuning={"dense_tiles": tiles})
+    ref, absagg, _ = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, rows=rows, want_lse=False)
+    if rows is not None:
+        got = got[rows]
+    assert np.all(np.isfinite(got))
+    err = gate_error(got, ref, absagg)
+    assert err <= TOL_BF16, "gate error %.3g" % err
+    return got
+
+
+@pytest.mark.parametrize("H,D", TILE_SHAPES)
+def test_tiles_irregular(H, D):
+    rowptr, colidx = irregular_block_graph(H * 100 + D)
+    Q, K, V = synth.features(H * 100 + D, rowptr.size - 1, H, D, "bf16")
+    scale = np.float32(1 / math.sqrt(D))
+    a = check(rowptr, colidx, Q, K, V, scale, tiles=256)
+    check(rowptr, colidx, Q, K, V, scale, tiles=1)
+    # the tile path really ran: its bf16-rounded weights change some outputs
+    # in dense windows, and none in the sparse window 9 (CSR kernel there)
+    csr = run_gpu(rowptr, colidx, Q, K, V, scale)
+    assert not np.array_equal(a[:64 * 9], csr[:64 * 9])
+    assert np.array_equal(a[64 * 9:64 * 10], csr[64 * 9:64 * 10])
+
+
+def test_tiles_single_entry_exact():
+    N, H, D = 64 * 8 + 5, 2, 64
+    rowptr = np.arange(N + 1, dtype=np.int64)
+    colidx = np.arange(N, dtype=np.int32)  # self-loop only: one in-window entry per row
+    Q, K, V = synth.features(21, N, H, D, "bf16", std=2.0)
+    got = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning={"dense_tiles": 1})
+    assert np.array_equal(got, bf16_bits_to_f32(V))
+
+
+def test_tiles_deterministic_and_off_equivalence():
+    rowptr, colidx = irregular_block_graph(22)
+    Q, K, V = synth.features(22, rowptr.size - 1, 2, 64, "bf16")
+    a = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning={"dense_tiles": 256})
+    b = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning={"dense_tiles": 256})
+    assert np.array_equal(a, b)
+    # a threshold no window reaches leaves everything to the CSR kernel
+    off = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125))
+    none = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning={"dense_tiles": 1 << 20})
+    assert np.array_equal(off, none)
+
+
+def test_tiles_ignored_for_fp32_and_wide_rows():
+    rowptr, colidx = irregular_block_graph(23)
+    N = rowptr.size - 1
+    Q, K, V = synth.features(23, N, 2, 64, "f32")
+    assert np.array_equal(run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125)),
+                          run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125),
+                                  tuning={"dense_tiles": 256}))
+    Qb, Kb, Vb = synth.features(23, N, 8, 64, "bf16")  # H*D = 512: no tile variant
+    assert np.array_equal(run_gpu(rowptr, colidx, Qb, Kb, Vb, np.float32(0.125)),
+                          run_gpu(rowptr, colidx, Qb, Kb, Vb, np.float32(0.125),
+                                  tuning={"dense_tiles": 256}))
+
+
+def test_tiles_full_sbm_sampled():
+    w = synth.config(3)
+    rows = sample_rows(w.rowptr, n_random=3000, n_top=64)
+    check(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, tiles=256, rows=rows)
