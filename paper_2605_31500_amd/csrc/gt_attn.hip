@@ -577,7 +577,9 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
     // ---- 1. staging
     if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
     for (int v = tid; v < kWin * (HD / 8); v += kBlock) {
-        const int cc = v / (HD / 8), e0 = (v % (HD / 8)) * 8;
+        // consecutive lanes take consecutive rows, so the transposed 2-byte
+        // writes of a wave land in consecutive LDS addresses
+        const int cc = v % kWin, e0 = (v / kWin) * 8;
         uint4 kx = make_uint4(0, 0, 0, 0), vx = make_uint4(0, 0, 0, 0);
         if (r0 + cc < p.N) {
             kx = *reinterpret_cast<const uint4*>(p.K + ((r0 + cc) * HD + e0) * 2);
