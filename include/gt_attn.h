@@ -132,11 +132,16 @@ typedef struct gt_tuning {
 /*
  * Generic entry: dtype selects fp32 (void* = float*) or bf16 (void* =
  * uint16_t*); tuning may be NULL (defaults).  Same contract as gt_attn_fwd.
+ * lse (may be NULL): device float [N][H], receives the natural-log
+ * logsumexp of each row's scaled scores, ln(sum_e exp(s_e)), -inf for an
+ * empty row -- the per-node statistic the paper stores so the backward pass
+ * can recompute the attention weights (Appendix D.2).  4-byte aligned, must
+ * not overlap the other buffers.
  */
 gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx,
-                         const void* Q, const void* K, const void* V, void* out, int64_t N,
-                         int64_t E, int32_t H, int32_t D, float scale, const gt_tuning* tuning,
-                         hipStream_t stream);
+                         const void* Q, const void* K, const void* V, void* out, float* lse,
+                         int64_t N, int64_t E, int32_t H, int32_t D, float scale,
+                         const gt_tuning* tuning, hipStream_t stream);
 
 /*
  * Debug utility, never on the attention path: checks on the device that

@@ -43,6 +43,13 @@ def _load():
                                     ctypes.c_int32, ctypes.c_int32, ctypes.c_float, P,
                                     ctypes.c_int64, P, P, P]
         L.gt_oracle_fwd.restype = ctypes.c_int
+        i64, i32 = ctypes.c_int64, ctypes.c_int32
+        L.gt_oracle_bwd_dq.argtypes = [ctypes.c_int, P, P, P, P, P, P, i64, i64, i32, i32,
+                                       ctypes.c_float, P, i64, P, P]
+        L.gt_oracle_bwd_dq.restype = ctypes.c_int
+        L.gt_oracle_bwd_dkv.argtypes = [ctypes.c_int, P, P, P, P, P, P, P, P, i64, i64, i32, i32,
+                                        ctypes.c_float, P, i64, P, P, P, P]
+        L.gt_oracle_bwd_dkv.restype = ctypes.c_int
         L.gt_oracle_threads.argtypes = []
         L.gt_oracle_threads.restype = ctypes.c_int
         _lib = L
@@ -91,3 +98,52 @@ def gt_attn_fwd(rowptr, colidx, Q, K, V, scale, rows=None, want_absagg=True, wan
     if rc == 2:
         raise ValueError("oracle: invalid CSR structure")
     return out, absagg, lse
+
+
+def _features(Q, K, V, extra=()):
+    arrs = [np.ascontiguousarray(x) for x in (Q, K, V) + tuple(extra)]
+    if any(a.dtype != arrs[0].dtype for a in arrs) or arrs[0].dtype not in (np.float32, np.uint16):
+        raise TypeError("features must all be float32 or all uint16 (bf16 bits)")
+    if any(a.shape != arrs[0].shape for a in arrs) or arrs[0].ndim != 3:
+        raise ValueError("features must share one [N, H, D] shape")
+    return arrs, (0 if arrs[0].dtype == np.float32 else 1)
+
+
+def gt_attn_bwd_dq(rowptr, colidx, Q, K, V, dO, scale, rows=None):
+    """dQ and its error scale (float64 [R, H, D] each) for the requested rows."""
+    rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
+    colidx = np.ascontiguousarray(colidx, dtype=np.int32)
+    (Q, K, V, dO), dtype = _features(Q, K, V, (dO,))
+    N, H, D = Q.shape
+    rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    nrows = N if rows is None else rows_arr.size
+    dQ = np.empty((nrows, H, D))
+    sdQ = np.empty_like(dQ)
+    rc = _load().gt_oracle_bwd_dq(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K), _ptr(V),
+                                  _ptr(dO), N, colidx.size, H, D, ctypes.c_float(float(scale)),
+                                  _ptr(rows_arr), nrows, _ptr(dQ), _ptr(sdQ))
+    if rc:
+        raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
+    return dQ, sdQ
+
+
+def gt_attn_bwd_dkv(rowptr, colidx, rowptr_t, colidx_t, Q, K, V, dO, scale, cols=None):
+    """dK, dV and their error scales (float64 [C, H, D] each) for the requested
+    source ids; rowptr_t/colidx_t is the transposed CSR (sources as rows)."""
+    rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
+    colidx = np.ascontiguousarray(colidx, dtype=np.int32)
+    rowptr_t = np.ascontiguousarray(rowptr_t, dtype=np.int64)
+    colidx_t = np.ascontiguousarray(colidx_t, dtype=np.int32)
+    (Q, K, V, dO), dtype = _features(Q, K, V, (dO,))
+    N, H, D = Q.shape
+    cols_arr = None if cols is None else np.ascontiguousarray(cols, dtype=np.int64)
+    ncols = N if cols is None else cols_arr.size
+    dK = np.empty((ncols, H, D))
+    dV, sdK, sdV = np.empty_like(dK), np.empty_like(dK), np.empty_like(dK)
+    rc = _load().gt_oracle_bwd_dkv(dtype, _ptr(rowptr), _ptr(colidx), _ptr(rowptr_t),
+                                   _ptr(colidx_t), _ptr(Q), _ptr(K), _ptr(V), _ptr(dO), N,
+                                   colidx.size, H, D, ctypes.c_float(float(scale)), _ptr(cols_arr),
+                                   ncols, _ptr(dK), _ptr(dV), _ptr(sdK), _ptr(sdV))
+    if rc:
+        raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
+    return dK, dV, sdK, sdV

@@ -128,3 +128,210 @@ int gt_oracle_fwd(int dtype, const int64_t* rowptr, const int32_t* colidx, const
     }
     return status ? 2 : 0;
 }
+
+/* ------------------------------------------------------------- backward
+ *
+ * Gradients of the same attention with respect to Q, K and V, for an upstream
+ * gradient dO [N][H][D] (same dtype as the features), in float64.  Followed
+ * from the paper's backward description (Appendix D.2, backward pass of the
+ * graph transformer): with the row statistic L_i = ln sum_e exp(s_e) the
+ * weights are recomputed as alpha_e = exp(s_e - L_i); with
+ * Delta_i = <O_i, dO_i> (O the exact forward output) and, per entry
+ * e = (i, j):
+ *     dalpha_e = <dO_i, V_j>,   ds_e = alpha_e * (dalpha_e - Delta_i)
+ *     dQ_i += scale * ds_e * K_j
+ *     dK_j += scale * ds_e * Q_i
+ *     dV_j += alpha_e * dO_i
+ * (all per head).  Alongside each gradient the routines return the same sums
+ * taken over absolute values of every factor (dalpha and Delta as sums of
+ * |products|), the scale of the rounding error of any evaluation.
+ */
+
+/* Row statistics of row i, head h: L (lse), o[D] (output), as the forward. */
+static void row_stats(int dtype, const int64_t* rowptr, const int32_t* colidx, const void* Q,
+                      const void* K, const void* V, int32_t H, int32_t D, double scale, int64_t i,
+                      int32_t h, double* L, double* o, double* s) {
+    const int64_t b = rowptr[i], e = rowptr[i + 1], deg = e - b;
+    for (int32_t d = 0; d < D; ++d) o[d] = 0.0;
+    if (deg == 0) { *L = -INFINITY; return; }
+    double m = -INFINITY;
+    for (int64_t t = 0; t < deg; ++t) {
+        const int64_t j = colidx[b + t];
+        double dot = 0.0;
+        for (int32_t d = 0; d < D; ++d)
+            dot += elem(Q, dtype, (i * H + h) * (int64_t)D + d) * elem(K, dtype, (j * H + h) * (int64_t)D + d);
+        s[t] = scale * dot;
+        if (s[t] > m) m = s[t];
+    }
+    double Z = 0.0;
+    for (int64_t t = 0; t < deg; ++t) {
+        const int64_t j = colidx[b + t];
+        const double w = exp(s[t] - m);
+        Z += w;
+        for (int32_t d = 0; d < D; ++d) o[d] += w * elem(V, dtype, (j * H + h) * (int64_t)D + d);
+    }
+    for (int32_t d = 0; d < D; ++d) o[d] /= Z;
+    *L = m + log(Z);
+}
+
+static int64_t max_degree(const int64_t* rowptr, int64_t N) {
+    int64_t mx = 0;
+    for (int64_t i = 0; i < N; ++i)
+        if (rowptr[i + 1] - rowptr[i] > mx) mx = rowptr[i + 1] - rowptr[i];
+    return mx;
+}
+
+/* dQ (and its error scale sdQ) for rows rows[0..nrows) (all rows if NULL). */
+int gt_oracle_bwd_dq(int dtype, const int64_t* rowptr, const int32_t* colidx, const void* Q,
+                     const void* K, const void* V, const void* dO, int64_t N, int64_t E, int32_t H,
+                     int32_t D, float scale, const int64_t* rows, int64_t nrows, double* dQ,
+                     double* sdQ) {
+    if ((dtype != ORACLE_F32 && dtype != ORACLE_BF16) || N < 0 || H < 1 || D < 1 || !rowptr ||
+        (E > 0 && !colidx) || (N > 0 && (!Q || !K || !V || !dO)) || (nrows > 0 && (!dQ || !sdQ)) ||
+        (!rows && nrows != N))
+        return 1;
+    if (rowptr[0] != 0 || rowptr[N] != E) return 2;
+    const double sc = (double)scale;
+    const int64_t maxdeg = max_degree(rowptr, N);
+    int status = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : status)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows ? rows[r] : r;
+        if (i < 0 || i >= N) { status |= 2; continue; }
+        double* s = (double*)malloc((size_t)(maxdeg > 0 ? maxdeg : 1) * sizeof(double));
+        double* o = (double*)malloc((size_t)D * sizeof(double));
+        const int64_t b = rowptr[i], deg = rowptr[i + 1] - b;
+        for (int32_t h = 0; h < H; ++h) {
+            double* g = dQ + (r * H + h) * (int64_t)D;
+            double* sg = sdQ + (r * H + h) * (int64_t)D;
+            for (int32_t d = 0; d < D; ++d) g[d] = sg[d] = 0.0;
+            if (deg == 0) continue;
+            double L;
+            row_stats(dtype, rowptr, colidx, Q, K, V, H, D, sc, i, h, &L, o, s);
+            double delta = 0.0, delta_abs = 0.0;
+            for (int32_t d = 0; d < D; ++d) {
+                const double go = elem(dO, dtype, (i * H + h) * (int64_t)D + d);
+                delta += o[d] * go;
+                delta_abs += fabs(o[d] * go);
+            }
+            for (int64_t t = 0; t < deg; ++t) {
+                const int64_t j = colidx[b + t];
+                const double alpha = exp(s[t] - L);
+                double da = 0.0, da_abs = 0.0;
+                for (int32_t d = 0; d < D; ++d) {
+                    const double p = elem(dO, dtype, (i * H + h) * (int64_t)D + d) *
+                                     elem(V, dtype, (j * H + h) * (int64_t)D + d);
+                    da += p;
+                    da_abs += fabs(p);
+                }
+                const double ds = alpha * (da - delta);
+                const double ds_abs = alpha * (da_abs + delta_abs);
+                for (int32_t d = 0; d < D; ++d) {
+                    const double kv = elem(K, dtype, (j * H + h) * (int64_t)D + d);
+                    g[d] += sc * ds * kv;
+                    sg[d] += fabs(sc) * ds_abs * fabs(kv);
+                }
+            }
+        }
+        free(o);
+        free(s);
+    }
+    return status ? 2 : 0;
+}
+
+/*
+ * dK, dV (and error scales) for source ids cols[0..ncols) (all if NULL),
+ * using the transposed structure rowptr_t/colidx_t: colidx_t lists, for
+ * source j, every destination row i whose CSR row holds j (once per entry).
+ */
+int gt_oracle_bwd_dkv(int dtype, const int64_t* rowptr, const int32_t* colidx,
+                      const int64_t* rowptr_t, const int32_t* colidx_t, const void* Q, const void* K,
+                      const void* V, const void* dO, int64_t N, int64_t E, int32_t H, int32_t D,
+                      float scale, const int64_t* cols, int64_t ncols, double* dK, double* dV,
+                      double* sdK, double* sdV) {
+    if ((dtype != ORACLE_F32 && dtype != ORACLE_BF16) || N < 0 || H < 1 || D < 1 || !rowptr ||
+        !rowptr_t || (E > 0 && (!colidx || !colidx_t)) || (N > 0 && (!Q || !K || !V || !dO)) ||
+        (ncols > 0 && (!dK || !dV || !sdK || !sdV)) || (!cols && ncols != N))
+        return 1;
+    if (rowptr[0] != 0 || rowptr[N] != E || rowptr_t[0] != 0 || rowptr_t[N] != E) return 2;
+    const double sc = (double)scale;
+    /* statistics (L, o, Delta) of every destination row that points at a requested source */
+    char* need = (char*)calloc((size_t)(N > 0 ? N : 1), 1);
+    for (int64_t c = 0; c < ncols; ++c) {
+        const int64_t j = cols ? cols[c] : c;
+        if (j < 0 || j >= N) { free(need); return 2; }
+        for (int64_t t = rowptr_t[j]; t < rowptr_t[j + 1]; ++t) {
+            if (colidx_t[t] < 0 || colidx_t[t] >= N) { free(need); return 2; }
+            need[colidx_t[t]] = 1;
+        }
+    }
+    int64_t* slot = (int64_t*)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    int64_t n_need = 0;
+    for (int64_t i = 0; i < N; ++i) slot[i] = need[i] ? n_need++ : -1;
+    int64_t* which = (int64_t*)malloc((size_t)(n_need > 0 ? n_need : 1) * sizeof(int64_t));
+    for (int64_t i = 0; i < N; ++i)
+        if (need[i]) which[slot[i]] = i;
+    double* Ls = (double*)malloc((size_t)(n_need > 0 ? n_need : 1) * H * sizeof(double));
+    double* Dl = (double*)malloc((size_t)(n_need > 0 ? n_need : 1) * H * sizeof(double));
+    double* Da = (double*)malloc((size_t)(n_need > 0 ? n_need : 1) * H * sizeof(double));
+    const int64_t maxdeg = max_degree(rowptr, N);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t u = 0; u < n_need; ++u) {
+        const int64_t i = which[u];
+        double* s = (double*)malloc((size_t)(maxdeg > 0 ? maxdeg : 1) * sizeof(double));
+        double* o = (double*)malloc((size_t)D * sizeof(double));
+        for (int32_t h = 0; h < H; ++h) {
+            row_stats(dtype, rowptr, colidx, Q, K, V, H, D, sc, i, h, &Ls[u * H + h], o, s);
+            double delta = 0.0, delta_abs = 0.0;
+            for (int32_t d = 0; d < D; ++d) {
+                const double go = elem(dO, dtype, (i * H + h) * (int64_t)D + d);
+                delta += o[d] * go;
+                delta_abs += fabs(o[d] * go);
+            }
+            Dl[u * H + h] = delta;
+            Da[u * H + h] = delta_abs;
+        }
+        free(o);
+        free(s);
+    }
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t c = 0; c < ncols; ++c) {
+        const int64_t j = cols ? cols[c] : c;
+        for (int32_t h = 0; h < H; ++h) {
+            double* gk = dK + (c * H + h) * (int64_t)D;
+            double* gv = dV + (c * H + h) * (int64_t)D;
+            double* sk = sdK + (c * H + h) * (int64_t)D;
+            double* sv = sdV + (c * H + h) * (int64_t)D;
+            for (int32_t d = 0; d < D; ++d) gk[d] = gv[d] = sk[d] = sv[d] = 0.0;
+            for (int64_t t = rowptr_t[j]; t < rowptr_t[j + 1]; ++t) {
+                const int64_t i = colidx_t[t], u = slot[i];
+                double dot = 0.0, da = 0.0, da_abs = 0.0;
+                for (int32_t d = 0; d < D; ++d) {
+                    dot += elem(Q, dtype, (i * H + h) * (int64_t)D + d) * elem(K, dtype, (j * H + h) * (int64_t)D + d);
+                    const double p = elem(dO, dtype, (i * H + h) * (int64_t)D + d) *
+                                     elem(V, dtype, (j * H + h) * (int64_t)D + d);
+                    da += p;
+                    da_abs += fabs(p);
+                }
+                const double alpha = exp(sc * dot - Ls[u * H + h]);
+                const double ds = alpha * (da - Dl[u * H + h]);
+                const double ds_abs = alpha * (da_abs + Da[u * H + h]);
+                for (int32_t d = 0; d < D; ++d) {
+                    const double qv = elem(Q, dtype, (i * H + h) * (int64_t)D + d);
+                    const double go = elem(dO, dtype, (i * H + h) * (int64_t)D + d);
+                    gk[d] += sc * ds * qv;
+                    sk[d] += fabs(sc) * ds_abs * fabs(qv);
+                    gv[d] += alpha * go;
+                    sv[d] += alpha * fabs(go);
+                }
+            }
+        }
+    }
+    free(Da);
+    free(Dl);
+    free(Ls);
+    free(which);
+    free(slot);
+    free(need);
+    return 0;
+}

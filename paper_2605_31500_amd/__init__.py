@@ -59,7 +59,7 @@ def load_library(path: str = LIB_PATH):
     sig = [P, P, P, P, P, P, i64, i64, i32, i32, f32, P]
     L.gt_attn_fwd.argtypes = sig
     L.gt_attn_fwd_bf16.argtypes = sig
-    L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:-1] + [ctypes.POINTER(GtTuning), P]
+    L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:6] + [P] + sig[6:-1] + [ctypes.POINTER(GtTuning), P]
     L.gt_csr_validate.argtypes = [P, P, i64, i64, ctypes.POINTER(i32), P]
     L.gt_status_string.argtypes = [ctypes.c_int]
     L.gt_status_string.restype = ctypes.c_char_p
@@ -130,8 +130,9 @@ def gt_attn_fwd_bf16(rowptr, colidx, Q, K, V, out, scale, stream=None) -> None:
                                            _stream(Q.device, stream)))
 
 
-def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None) -> None:
-    """Either dtype (taken from Q); tuning: dict or GtTuning of partition overrides."""
+def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None, lse=None) -> None:
+    """Either dtype (taken from Q); tuning: dict or GtTuning of partition overrides;
+    lse: optional float32 [N, H] device tensor receiving ln(sum_e exp(s_e)) per row."""
     if Q.dtype == torch.float32:
         dtype, allowed = GT_DTYPE_F32, (torch.float32,)
     else:
@@ -141,19 +142,26 @@ def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None
     if isinstance(tuning, dict):
         tuning = GtTuning(**tuning)
     tp = ctypes.byref(tuning) if tuning is not None else None
+    if lse is not None:
+        if not (lse.is_cuda and lse.is_contiguous() and lse.dtype == torch.float32
+                and tuple(lse.shape) == (N, H)):
+            raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
     _check(load_library().gt_attn_fwd_ex(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
-                                         _ptr(V), _ptr(out), N, colidx.numel(), H, D,
+                                         _ptr(V), _ptr(out), _ptr(lse), N, colidx.numel(), H, D,
                                          float(scale), tp, _stream(Q.device, stream)))
 
 
-def attention(rowptr, colidx, Q, K, V, scale=None, tuning=None, out=None, stream=None):
-    """Convenience: allocates ``out`` like Q and dispatches on Q's dtype."""
+def attention(rowptr, colidx, Q, K, V, scale=None, tuning=None, out=None, stream=None,
+              return_lse=False):
+    """Convenience: allocates ``out`` like Q (and ``lse`` when asked) and
+    dispatches on Q's dtype."""
     if out is None:
         out = torch.empty_like(Q)
     if scale is None:
         scale = Q.shape[-1] ** -0.5
-    gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=tuning, stream=stream)
-    return out
+    lse = torch.empty(Q.shape[:2], dtype=torch.float32, device=Q.device) if return_lse else None
+    gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=tuning, stream=stream, lse=lse)
+    return (out, lse) if return_lse else out
 
 
 def gt_csr_validate(rowptr, colidx, stream=None) -> bool:

@@ -109,6 +109,7 @@ struct AttnParams {
     const char* K;
     const char* V;
     char* out;
+    float* lse;  // [N][H] natural-log logsumexp of the scaled scores, or nullptr
     int64_t N;
     float c;  // scale * log2(e)
     int32_t light_max;
@@ -143,6 +144,7 @@ struct MergeParams {
     const float* part_acc;
     const float2* part_ml;
     char* out;
+    float* lse;
 };
 
 // ------------------------------------------------------------ element codecs
@@ -213,6 +215,12 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
+}
+
+// ln(sum_e exp(s_e)) from the running state in base-2 units: the sum is
+// 2^m * l, so the logarithm is (m + log2 l) * ln 2; -inf for an empty row.
+__device__ __forceinline__ float lse_of(float m, float l) {
+    return l > 0.0f ? (m + log2f(l)) * 0.6931471805599453f : -INFINITY;
 }
 
 // ------------------------------------------------------------ per-lane state
@@ -329,7 +337,8 @@ struct RowState {
         }
     }
 
-    __device__ __forceinline__ void store_out(char* __restrict__ outb, int64_t row, int lig) const {
+    __device__ __forceinline__ void store_out(char* __restrict__ outb, float* __restrict__ lse, int64_t row,
+                                              int lig) const {
         char* orow = outb + row * (int64_t)Gm::kRowBytes + lig * 16;
 #pragma unroll
         for (int k = 0; k < Gm::kNV; ++k) {
@@ -338,6 +347,8 @@ struct RowState {
 #pragma unroll
             for (int e = 0; e < Gm::kEPV; ++e) o[e] = acc[k][e] * inv;
             *reinterpret_cast<uint4*>(orow + k * Gm::kG * 16) = narrow<T>(o);
+            const int v = lig + k * Gm::kG;
+            if (lse && v % Gm::kHL == 0) lse[row * H + v / Gm::kHL] = lse_of(m[k], l[k]);
         }
     }
 
@@ -388,7 +399,7 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
     for (int off = G; off < kWave; off <<= 1) st.merge_xor(off);
     if (g == 0) {
         if (slot < 0)
-            st.store_out(p.out, row, lig);
+            st.store_out(p.out, p.lse, row, lig);
         else
             st.store_partial(p.part_acc, p.part_ml, slot, lig);
     }
@@ -445,7 +456,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
                     st.consume(bt, nvalid, p.c);
                 }
             }
-            st.store_out(p.out, crow, lig);
+            st.store_out(p.out, p.lse, crow, lig);
         }
         if (!fetched) idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
     }
@@ -527,6 +538,7 @@ struct TileParams {
     const char* K;
     const char* V;
     char* out;
+    float* lse;
     int64_t N;
     float c;  // scale * log2(e)
     int32_t light_max;  // <= kWinMaxDeg
@@ -807,7 +819,7 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
             st.step(p.K, p.V, j, nvalid, lig, p.c);
         }
         wave_lds_fence();
-        st.store_out(p.out, row, lig);
+        st.store_out(p.out, p.lse, row, lig);
     }
 }
 
@@ -969,6 +981,7 @@ __global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
             }
         }
         const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+        if (p.lse && f0 % D == 0) p.lse[(int64_t)w.row * H + head] = lse_of(m, l);
         char* orow = p.out + (int64_t)w.row * HD * EB;
 #pragma unroll
         for (int f = 0; f < F; ++f) {
@@ -1066,6 +1079,7 @@ struct Args {
     const void* K;
     const void* V;
     void* out;
+    float* lse;
     int64_t N, E;
     int32_t H, D;
     float scale;
@@ -1220,6 +1234,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
             tp.K = static_cast<const char*>(a.K);
             tp.V = static_cast<const char*>(a.V);
             tp.out = static_cast<char*>(a.out);
+            tp.lse = a.lse;
             tp.N = a.N;
             tp.c = a.scale * 1.4426950408889634f;
             tp.light_max = light_max;
@@ -1238,6 +1253,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.K = static_cast<const char*>(a.K);
     ap.V = static_cast<const char*>(a.V);
     ap.out = static_cast<char*>(a.out);
+    ap.lse = a.lse;
     ap.N = a.N;
     ap.c = a.scale * 1.4426950408889634f;
     ap.light_max = light_max;
@@ -1260,6 +1276,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     mp.part_acc = ap.part_acc;
     mp.part_ml = ap.part_ml;
     mp.out = ap.out;
+    mp.lse = a.lse;
     int merge_grid = (int)((cap_heavy + kWavesPerBlock - 1) / kWavesPerBlock);
     const int merge_cap = device_cus(dev) * 8;
     if (merge_grid > merge_cap) merge_grid = merge_cap;
@@ -1316,6 +1333,12 @@ gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t st
     const size_t bytes = (size_t)a.N * a.H * a.D * (dtype == GT_DTYPE_F32 ? 4 : 2);
     for (const void* in : {a.Q, a.K, a.V})
         if (overlaps(a.out, bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "out overlaps Q, K or V");
+    if (a.lse) {
+        const size_t lb = (size_t)a.N * a.H * sizeof(float);
+        if (reinterpret_cast<uintptr_t>(a.lse) % 4 != 0) return fail(GT_ERROR_INVALID_VALUE, "lse must be 4-byte aligned");
+        for (const void* o : {a.Q, a.K, a.V, static_cast<const void*>(a.out)})
+            if (overlaps(a.lse, lb, o, bytes)) return fail(GT_ERROR_INVALID_VALUE, "lse overlaps Q, K, V or out");
+    }
     return fn(a, tu, stream);
 }
 
@@ -1326,19 +1349,19 @@ extern "C" {
 gt_status gt_attn_fwd(const int64_t* rowptr, const int32_t* colidx, const float* Q, const float* K,
                       const float* V, float* out, int64_t N, int64_t E, int32_t H, int32_t D, float scale,
                       hipStream_t stream) {
-    return run(GT_DTYPE_F32, Args{rowptr, colidx, Q, K, V, out, N, E, H, D, scale}, nullptr, stream);
+    return run(GT_DTYPE_F32, Args{rowptr, colidx, Q, K, V, out, nullptr, N, E, H, D, scale}, nullptr, stream);
 }
 
 gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const uint16_t* Q, const uint16_t* K,
                            const uint16_t* V, uint16_t* out, int64_t N, int64_t E, int32_t H, int32_t D,
                            float scale, hipStream_t stream) {
-    return run(GT_DTYPE_BF16, Args{rowptr, colidx, Q, K, V, out, N, E, H, D, scale}, nullptr, stream);
+    return run(GT_DTYPE_BF16, Args{rowptr, colidx, Q, K, V, out, nullptr, N, E, H, D, scale}, nullptr, stream);
 }
 
 gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const void* Q,
-                         const void* K, const void* V, void* out, int64_t N, int64_t E, int32_t H, int32_t D,
-                         float scale, const gt_tuning* tuning, hipStream_t stream) {
-    return run(dtype, Args{rowptr, colidx, Q, K, V, out, N, E, H, D, scale}, tuning, stream);
+                         const void* K, const void* V, void* out, float* lse, int64_t N, int64_t E, int32_t H,
+                         int32_t D, float scale, const gt_tuning* tuning, hipStream_t stream) {
+    return run(dtype, Args{rowptr, colidx, Q, K, V, out, lse, N, E, H, D, scale}, tuning, stream);
 }
 
 gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t N, int64_t E, int32_t* valid,

@@ -313,3 +313,14 @@ def ragged_graph(seed: int, N: int, max_deg: int, empty_frac: float = 0.1, hubs=
         order = np.lexsort((us, row_of))
         colidx = colidx[order].copy()
     return rowptr, colidx
+
+
+def transpose_csr(rowptr: np.ndarray, colidx: np.ndarray, N: int):
+    """Transposed structure: row j lists every destination i whose row holds j
+    (one entry per CSR entry, destinations in increasing order)."""
+    rows = np.repeat(np.arange(N, dtype=np.int32), np.diff(rowptr))
+    order = np.argsort(colidx, kind="stable")
+    colidx_t = np.ascontiguousarray(rows[order])
+    rowptr_t = np.zeros(N + 1, dtype=np.int64)
+    np.cumsum(np.bincount(colidx, minlength=N), out=rowptr_t[1:])
+    return rowptr_t, colidx_t

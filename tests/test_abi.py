@@ -42,10 +42,10 @@ FAKE = 0x10000  # never dereferenced: each call below fails validation first
 
 
 def call(lib, dtype=0, rowptr=FAKE, colidx=FAKE, Q=FAKE, K=FAKE + 0x100000, V=FAKE + 0x200000,
-         out=FAKE + 0x300000, N=10, E=20, H=4, D=32, scale=0.1):
+         out=FAKE + 0x300000, lse=None, N=10, E=20, H=4, D=32, scale=0.1):
     P = ctypes.c_void_p
-    return lib.gt_attn_fwd_ex(dtype, P(rowptr), P(colidx), P(Q), P(K), P(V), P(out), N, E, H, D,
-                              ctypes.c_float(scale), None, None)
+    return lib.gt_attn_fwd_ex(dtype, P(rowptr), P(colidx), P(Q), P(K), P(V), P(out), P(lse), N, E,
+                              H, D, ctypes.c_float(scale), None, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -56,6 +56,8 @@ def call(lib, dtype=0, rowptr=FAKE, colidx=FAKE, Q=FAKE, K=FAKE + 0x100000, V=FA
     (dict(K=FAKE + 8), 1),                      # misaligned
     (dict(out=FAKE + 0x200000 + 1024), 1),      # out overlaps V
     (dict(out=FAKE), 1),                        # out aliases Q
+    (dict(lse=FAKE + 0x300000 + 4), 1),         # lse overlaps out
+    (dict(lse=FAKE + 0x400002), 1),             # lse misaligned
 ])
 def test_host_validation(lib, kw, status):
     assert call(lib, **kw) == status

@@ -27,7 +27,15 @@ MUTANTS = {
     "absagg_signed": ("if (a) a[d] += w * fabs(v);", "if (a) a[d] += w * v;"),
     "bf16_widening": ("uint32_t bits = (uint32_t)((const uint16_t*)base)[k] << 16;",
                       "uint32_t bits = (uint32_t)((const uint16_t*)base)[k] << 15;"),
+    "bwd_drops_delta": ("const double ds = alpha * (da - delta);", "const double ds = alpha * da;"),
+    "bwd_dkv_drops_delta": ("const double ds = alpha * (da - Dl[u * H + h]);",
+                            "const double ds = alpha * da;"),
+    "bwd_alpha_without_lse": ("const double alpha = exp(s[t] - L);", "const double alpha = exp(s[t]);"),
+    "bwd_dk_without_scale": ("gk[d] += sc * ds * qv;", "gk[d] += ds * qv;"),
+    "bwd_dv_without_alpha": ("gv[d] += alpha * go;", "gv[d] += go;"),
+    "bwd_dq_sign": ("g[d] += sc * ds * kv;", "g[d] -= sc * ds * kv;"),
 }
+PIN_FILES = ["test_oracle_pins.py", "test_oracle_bwd_pins.py"]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
@@ -40,9 +48,10 @@ def test_pins_reject_mutant(name, tmp_path):
     so = tmp_path / "libgt_oracle.so"
     subprocess.run(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", str(csrc), "-o",
                     str(so), "-lm"], check=True)
+    files = [os.path.join(ROOT, "tests", f) for f in PIN_FILES]
     code = ("import sys, oracle, pytest; oracle._SO = %r; "
-            "sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider', %r]))"
-            % (str(so), os.path.join(ROOT, "tests", "test_oracle_pins.py")))
+            "sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider'] + %r))"
+            % (str(so), files))
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
                        env=dict(os.environ, OMP_NUM_THREADS="2"))
     assert r.returncode != 0, "pins accepted a planted mistake: " + name
