@@ -144,6 +144,30 @@ gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* c
                          const gt_tuning* tuning, hipStream_t stream);
 
 /*
+ * Backward pass (paper Appendix D.2, backward of the graph transformer):
+ * gradients dQ, dK, dV of sum(out * dout) for the forward defined above.
+ * The attention weights are recomputed from lse, the forward's per-row
+ * statistic (gt_attn_fwd_ex), as alpha_e = exp(s_e - lse_i); with
+ * Delta_i = <out_i, dout_i> per head and ds_e = alpha_e (<dout_i, V_j> - Delta_i):
+ *     dQ_i = scale sum_e ds_e K_j,   dK_j = scale sum_e ds_e Q_i,
+ *     dV_j = sum_e alpha_e dout_i    (e = (i, j) over CSR entries).
+ * rowptr_t / colidx_t is the transposed structure: row j lists, once per
+ * CSR entry, every destination i whose row holds j (the order within a row
+ * fixes the summation order; a fixed structure gives bitwise-reproducible
+ * gradients).  out and lse must come from the forward of the same inputs.
+ * Layouts: Q, K, V, out, dout, dQ, dK, dV [N][H][D] in `dtype`, 16-byte
+ * aligned; lse float [N][H].  Gradients are accumulated in fp32 and written
+ * in `dtype` (bf16 rounded to nearest even); they must not overlap the
+ * inputs or each other.  Asynchronous on `stream`; uses the stream's cached
+ * workspace.
+ */
+gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx,
+                      const int64_t* rowptr_t, const int32_t* colidx_t, const void* Q,
+                      const void* K, const void* V, const void* out, const void* dout,
+                      const float* lse, void* dQ, void* dK, void* dV, int64_t N, int64_t E,
+                      int32_t H, int32_t D, float scale, hipStream_t stream);
+
+/*
  * Debug utility, never on the attention path: checks on the device that
  * rowptr[0] == 0, rowptr is non-decreasing, rowptr[N] == E and every colidx
  * entry lies in [0, N).  Synchronous on `stream`; *valid (host memory) is set

@@ -25,7 +25,7 @@ GT_DTYPE_F32 = 0
 GT_DTYPE_BF16 = 1
 
 EXPORTED_SYMBOLS = (
-    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_csr_validate", "gt_status_string",
+    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_attn_bwd", "gt_csr_validate", "gt_status_string",
     "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
 )
 
@@ -60,6 +60,8 @@ def load_library(path: str = LIB_PATH):
     L.gt_attn_fwd.argtypes = sig
     L.gt_attn_fwd_bf16.argtypes = sig
     L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:6] + [P] + sig[6:-1] + [ctypes.POINTER(GtTuning), P]
+    L.gt_attn_bwd.argtypes = [ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, P, i64, i64, i32, i32,
+                              f32, P]
     L.gt_csr_validate.argtypes = [P, P, i64, i64, ctypes.POINTER(i32), P]
     L.gt_status_string.argtypes = [ctypes.c_int]
     L.gt_status_string.restype = ctypes.c_char_p
@@ -68,7 +70,7 @@ def load_library(path: str = LIB_PATH):
     L.gt_profile_enable.argtypes = [i32]
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     L.gt_workspace_release.argtypes = []
-    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_csr_validate",
+    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_attn_bwd", "gt_csr_validate",
                  "gt_profile_enable", "gt_profile_collect", "gt_workspace_release"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -149,6 +151,29 @@ def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None
     _check(load_library().gt_attn_fwd_ex(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
                                          _ptr(V), _ptr(out), _ptr(lse), N, colidx.numel(), H, D,
                                          float(scale), tp, _stream(Q.device, stream)))
+
+
+def gt_attn_bwd(rowptr, colidx, rowptr_t, colidx_t, Q, K, V, out, dout, lse, dQ, dK, dV, scale,
+                stream=None) -> None:
+    """Gradients of sum(out * dout); see include/gt_attn.h.  rowptr_t/colidx_t
+    is the transposed structure (sources as rows)."""
+    if Q.dtype == torch.float32:
+        dtype, allowed = GT_DTYPE_F32, (torch.float32,)
+    else:
+        dtype, allowed = GT_DTYPE_BF16, (torch.bfloat16, torch.int16, torch.uint16)
+    _check_tensors(rowptr, colidx, Q, K, V, out, allowed)
+    _check_tensors(rowptr_t, colidx_t, dout, dQ, dK, dV, allowed)
+    N, H, D = Q.shape
+    if colidx_t.numel() != colidx.numel():
+        raise ValueError("the transposed structure must have as many entries as the CSR")
+    if not (lse.is_cuda and lse.is_contiguous() and lse.dtype == torch.float32
+            and tuple(lse.shape) == (N, H)):
+        raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
+    _check(load_library().gt_attn_bwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(rowptr_t),
+                                      _ptr(colidx_t), _ptr(Q), _ptr(K), _ptr(V), _ptr(out),
+                                      _ptr(dout), _ptr(lse), _ptr(dQ), _ptr(dK), _ptr(dV), N,
+                                      colidx.numel(), H, D, float(scale),
+                                      _stream(Q.device, stream)))
 
 
 def attention(rowptr, colidx, Q, K, V, scale=None, tuning=None, out=None, stream=None,

@@ -1342,6 +1342,44 @@ gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t st
     return fn(a, tu, stream);
 }
 
+#include "gt_bwd.hpp"
+
+gt_status run_bwd(gt_dtype dtype, const BwdArgs& a, hipStream_t stream) {
+    t_last_error.clear();
+    if (dtype != GT_DTYPE_F32 && dtype != GT_DTYPE_BF16) return fail(GT_ERROR_NOT_SUPPORTED, "unknown dtype");
+    if (a.N < 0 || a.N >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "N must be in [0, 2^31)");
+    if (a.E < 0 || a.E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
+    if (a.H < 1 || a.D < 1) return fail(GT_ERROR_INVALID_VALUE, "H and D must be positive");
+    if (!std::isfinite(a.scale)) return fail(GT_ERROR_INVALID_VALUE, "scale must be finite");
+    BwdFn fn = dtype == GT_DTYPE_F32 ? pick_bwd<float>(a.H, a.D) : pick_bwd<bf16_tag>(a.H, a.D);
+    if (!fn)
+        return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +
+                                                std::to_string(a.D) + "); H in {1,2,4,8}, D in {32,64,128}");
+    if (a.N == 0) return GT_SUCCESS;
+    if (!a.rowptr || !a.rowptr_t) return fail(GT_ERROR_INVALID_VALUE, "rowptr or rowptr_t is null");
+    if (a.E > 0 && (!a.colidx || !a.colidx_t)) return fail(GT_ERROR_INVALID_VALUE, "colidx or colidx_t is null");
+    const void* ins[] = {a.Q, a.K, a.V, a.O, a.dO};
+    const void* outs[] = {a.dQ, a.dK, a.dV};
+    for (const void* ptr : ins)
+        if (!ptr || reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
+            return fail(GT_ERROR_INVALID_VALUE, "Q, K, V, out and dout must be non-null and 16-byte aligned");
+    for (const void* ptr : outs)
+        if (!ptr || reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
+            return fail(GT_ERROR_INVALID_VALUE, "dQ, dK and dV must be non-null and 16-byte aligned");
+    if (!a.lse || reinterpret_cast<uintptr_t>(a.lse) % 4 != 0)
+        return fail(GT_ERROR_INVALID_VALUE, "lse must be non-null and 4-byte aligned");
+    const size_t bytes = (size_t)a.N * a.H * a.D * (dtype == GT_DTYPE_F32 ? 4 : 2);
+    for (const void* o : outs) {
+        for (const void* in : ins)
+            if (overlaps(o, bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "a gradient overlaps an input");
+        if (overlaps(o, bytes, a.lse, (size_t)a.N * a.H * sizeof(float)))
+            return fail(GT_ERROR_INVALID_VALUE, "a gradient overlaps lse");
+        for (const void* o2 : outs)
+            if (o2 != o && overlaps(o, bytes, o2, bytes)) return fail(GT_ERROR_INVALID_VALUE, "gradients overlap");
+    }
+    return fn(a, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1362,6 +1400,15 @@ gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* c
                          const void* K, const void* V, void* out, float* lse, int64_t N, int64_t E, int32_t H,
                          int32_t D, float scale, const gt_tuning* tuning, hipStream_t stream) {
     return run(dtype, Args{rowptr, colidx, Q, K, V, out, lse, N, E, H, D, scale}, tuning, stream);
+}
+
+gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const int64_t* rowptr_t,
+                      const int32_t* colidx_t, const void* Q, const void* K, const void* V, const void* out,
+                      const void* dout, const float* lse, void* dQ, void* dK, void* dV, int64_t N, int64_t E,
+                      int32_t H, int32_t D, float scale, hipStream_t stream) {
+    return run_bwd(dtype,
+                   BwdArgs{rowptr, colidx, rowptr_t, colidx_t, Q, K, V, out, dout, lse, dQ, dK, dV, N, E, H, D, scale},
+                   stream);
 }
 
 gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t N, int64_t E, int32_t* valid,

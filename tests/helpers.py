@@ -132,3 +132,21 @@ def sample_rows(rowptr: np.ndarray, n_random: int, n_top: int, seed: int = 0) ->
         if hit.size:
             extra.append(int(hit[0]))
     return np.unique(np.concatenate([top, rnd, np.array(extra, dtype=np.int64)]))
+
+
+def run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, scale, tuning=None):
+    """Forward (with lse) then backward through the C ABI; float32 host results
+    (out, lse, dQ, dK, dV)."""
+    import torch
+    import paper_2605_31500_amd as gt
+    import synth
+    N, H, D = Q.shape
+    rpt, cit = synth.transpose_csr(rowptr, colidx, N)
+    rp, ci, rpt_d, cit_d, q, k, v, do = (to_device(x) for x in (rowptr, colidx, rpt, cit, Q, K, V, dO))
+    out = torch.empty_like(q)
+    lse = torch.empty((N, H), dtype=torch.float32, device=q.device)
+    gt.gt_attn_fwd_ex(rp, ci, q, k, v, out, scale, tuning=tuning, lse=lse)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    gt.gt_attn_bwd(rp, ci, rpt_d, cit_d, q, k, v, out, do, lse, dq, dk, dv, scale)
+    torch.cuda.synchronize()
+    return (to_host_f32(out), lse.cpu().numpy(), to_host_f32(dq), to_host_f32(dk), to_host_f32(dv))

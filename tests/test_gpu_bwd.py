@@ -1,0 +1,119 @@
+"""GPU parity of the logsumexp output and of the backward pass (Appendix D.2
+of the paper: weights recomputed from the stored row statistic) against the
+float64 oracle.  Gradient gate: max |x - r| / max(|r|, S) with S the same sums
+over absolute values of every factor (returned by the oracle); 1e-5 for fp32,
+2e-2 for bf16."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.helpers import (TOL_BF16, TOL_F32, gate_error, run_gpu_fwd_bwd, sample_rows)
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(h, d) for h in (1, 2, 4, 8) for d in (32, 64, 128)]
+FORCED_SPLIT = {"light_max_deg": 2, "heavy_min_deg": 6, "chunk_edges": 64, "grid_blocks": 0}
+
+
+def tol(dtype):
+    return TOL_F32 if dtype == "f32" else TOL_BF16
+
+
+def check_lse(lse, ref, atol):
+    fin = np.isfinite(ref)
+    assert np.array_equal(np.isneginf(lse), ~fin)
+    assert np.all(np.abs(lse[fin] - ref[fin]) <= atol * np.maximum(1.0, np.abs(ref[fin])))
+
+
+def check_grads(rowptr, colidx, Q, K, V, dO, scale, got, dtype, rows=None, cols=None):
+    _, _, dq, dk, dv = got
+    N = Q.shape[0]
+    rpt, cit = synth.transpose_csr(rowptr, colidx, N)
+    rq, sq = oracle.gt_attn_bwd_dq(rowptr, colidx, Q, K, V, dO, scale, rows=rows)
+    rk, rv, sk, sv = oracle.gt_attn_bwd_dkv(rowptr, colidx, rpt, cit, Q, K, V, dO, scale, cols=cols)
+    if rows is not None:
+        dq = dq[rows]
+    if cols is not None:
+        dk, dv = dk[cols], dv[cols]
+    for name, x, r, sc in (("dQ", dq, rq, sq), ("dK", dk, rk, sk), ("dV", dv, rv, sv)):
+        assert np.all(np.isfinite(x)), name
+        err = gate_error(x, r, sc)
+        assert err <= tol(dtype), "%s gate error %.3g" % (name, err)
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("H,D", SHAPES)
+def test_lse_and_backward_small(H, D, dtype, split):
+    N = 300
+    seed = 7000 + H * 100 + D
+    rowptr, colidx = synth.ragged_graph(seed, N, max_deg=24, empty_frac=0.1,
+                                        hubs={7: 299, 100: 150, 299: 70}, self_loops=True,
+                                        dup_frac=0.05, shuffle=True)
+    Q, K, V = synth.features(seed, N, H, D, dtype)
+    dO, _, _ = synth.features(seed + 1, N, H, D, dtype)
+    scale = np.float32(1 / math.sqrt(D))
+    got = run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, scale,
+                          tuning=FORCED_SPLIT if split else None)
+    _, _, ref_lse = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, want_absagg=False)
+    check_lse(got[1], ref_lse, 1e-5)
+    check_grads(rowptr, colidx, Q, K, V, dO, scale, got, dtype)
+
+
+def test_backward_deterministic():
+    N, H, D = 5000, 4, 32
+    rowptr, colidx = synth.ragged_graph(31, N, max_deg=30, hubs={1: 4999, 2: 3000})
+    Q, K, V = synth.features(31, N, H, D, "f32")
+    dO, _, _ = synth.features(32, N, H, D, "f32")
+    a = run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, np.float32(0.2))
+    b = run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, np.float32(0.2))
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_entry_rows_zero_query_key_gradients(dtype):
+    N, H, D = 3000, 4, 32
+    rowptr, colidx = synth.csr_from_degrees(33, N, np.ones(N, dtype=np.int64), self_loops=False)
+    Q, K, V = synth.features(33, N, H, D, dtype)
+    dO, _, _ = synth.features(34, N, H, D, dtype)
+    got = run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, np.float32(0.3))
+    assert np.all(got[2] == 0) and np.all(got[3] == 0)
+    check_grads(rowptr, colidx, Q, K, V, dO, np.float32(0.3), got, dtype)
+
+
+def test_lse_tile_mode():
+    w_rp, w_ci = synth.sbm_graph(35, 64 * 20 + 9, 64, 4)
+    N = w_rp.size - 1
+    Q, K, V = synth.features(35, N, 2, 64, "bf16")
+    dO, _, _ = synth.features(36, N, 2, 64, "bf16")
+    got = run_gpu_fwd_bwd(w_rp, w_ci, Q, K, V, dO, np.float32(0.125), tuning={"dense_tiles": 256})
+    _, _, ref_lse = oracle.gt_attn_fwd(w_rp, w_ci, Q, K, V, np.float32(0.125), want_absagg=False)
+    check_lse(got[1], ref_lse, 4e-3)  # tile weights are rounded to bf16
+
+
+def test_full_config_power_law_all_rows():
+    w = synth.config(1)
+    dO, _, _ = synth.features(37, w.N, w.H, w.D, w.dtype)
+    got = run_gpu_fwd_bwd(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale)
+    _, _, ref_lse = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_absagg=False)
+    check_lse(got[1], ref_lse, 1e-5)
+    check_grads(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale, got, w.dtype)
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4])
+def test_full_config_sampled(idx):
+    w = synth.config(idx)
+    print("config", idx, w.name, flush=True)
+    dO, _, _ = synth.features(38, w.N, w.H, w.D, w.dtype)
+    got = run_gpu_fwd_bwd(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale)
+    rows = sample_rows(w.rowptr, n_random=1500, n_top=32)
+    rpt, _ = synth.transpose_csr(w.rowptr, w.colidx, w.N)
+    cols = sample_rows(rpt, n_random=1500, n_top=32, seed=1)
+    _, _, ref_lse = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, rows=rows,
+                                       want_absagg=False)
+    check_lse(got[1][rows], ref_lse, 1e-5)
+    check_grads(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale, got, w.dtype, rows=rows, cols=cols)
