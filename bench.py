@@ -40,6 +40,60 @@ def compulsory_bytes(w) -> int:
     return 8 * (w.N + 1) + 4 * w.E + 4 * w.N * R
 
 
+def backward_model_bytes(w) -> int:
+    """Per-edge byte model of the backward: pass 1 gathers K, V per entry and
+    reads Q, dO, out, lse and writes dQ per row; pass 2 gathers Q, dO and the
+    row statistics (lse, Delta) per entry of the transposed structure and reads
+    K, V and writes dK, dV per row; both read their row pointers and indices."""
+    eb = 4 if w.dtype == "f32" else 2
+    R = w.H * w.D * eb
+    idx = 2 * (8 * (w.N + 1) + 4 * w.E)
+    pass1 = w.E * 2 * R + w.N * (4 * R + 4 * w.H + 4 * w.H)
+    pass2 = w.E * (2 * R + 8 * w.H) + w.N * 4 * R
+    return idx + pass1 + pass2
+
+
+def run_backward(args, w, gt, torch, to_device, synth) -> dict:
+    rpt, cit = synth.transpose_csr(w.rowptr, w.colidx, w.N)
+    dO, _, _ = synth.features(1, w.N, w.H, w.D, w.dtype)
+    rp, ci, rpt_d, cit_d, q, k, v, do = (to_device(x) for x in (w.rowptr, w.colidx, rpt, cit, w.Q,
+                                                              w.K, w.V, dO))
+    out = torch.empty_like(q)
+    lse = torch.empty((w.N, w.H), dtype=torch.float32, device=q.device)
+    gt.gt_attn_fwd_ex(rp, ci, q, k, v, out, w.scale, lse=lse)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gt.gt_attn_bwd(rp, ci, rpt_d, cit_d, q, k, v, out, do, lse, dq, dk, dv, w.scale,
+                       stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    mbytes = backward_model_bytes(w)
+    achieved = mbytes / (ms * 1e-3) / 1e9
+    return {
+        "metric": "fused graph-attention bwd GEdges/s at 1 MI355X; achieved HBM GB/s vs peak",
+        "value": round(w.E / (ms * 1e-3) / 1e9, 4), "unit": "GEdges/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic", "config": w.describe(),
+        "roofline": {"bound": "hbm", "kernel": "gt_attn_bwd (whole call: 2 passes)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": mbytes, "kernel_ms": round(ms, 5)},
+    }
+
+
 def source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
@@ -95,6 +149,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=1, help="workload index 0..4 (default 1)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward pass (gt_attn_bwd) instead of the forward")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
                     help="enable the matrix-core path for dense 64-id windows holding at "
                          "least MIN in-window entries (bf16, H*D <= 128)")
@@ -119,6 +175,9 @@ def main() -> int:
     from tests.helpers import to_device
 
     w = synth.config(args.config)
+    if args.backward:
+        print(json.dumps(run_backward(args, w, gt, torch, to_device, synth)), flush=True)
+        return 0
     dev = [to_device(x) for x in (w.rowptr, w.colidx, w.Q, w.K, w.V)]
     out = torch.empty_like(dev[2])
     stream = torch.cuda.current_stream()
