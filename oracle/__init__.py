@@ -50,6 +50,9 @@ def _load():
         L.gt_oracle_bwd_dkv.argtypes = [ctypes.c_int, P, P, P, P, P, P, P, P, i64, i64, i32, i32,
                                         ctypes.c_float, P, i64, P, P, P, P]
         L.gt_oracle_bwd_dkv.restype = ctypes.c_int
+        L.gt_oracle_gatv2_fwd.argtypes = [ctypes.c_int, P, P, P, P, P, i64, i64, i32, i32,
+                                          ctypes.c_float, P, i64, P, P, P]
+        L.gt_oracle_gatv2_fwd.restype = ctypes.c_int
         L.gt_oracle_threads.argtypes = []
         L.gt_oracle_threads.restype = ctypes.c_int
         _lib = L
@@ -147,3 +150,27 @@ def gt_attn_bwd_dkv(rowptr, colidx, rowptr_t, colidx_t, Q, K, V, dO, scale, cols
     if rc:
         raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
     return dK, dV, sdK, sdV
+
+
+def gatv2_fwd(rowptr, colidx, Lf, Rf, att, slope, rows=None, want_absagg=True, want_lse=True):
+    """GATv2 reference forward.  Lf, Rf: [N,H,D] float32 or uint16 bf16 bits;
+    att: [H,D] float32; slope: LeakyReLU negative slope.  Returns (out, absagg, lse)."""
+    rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
+    colidx = np.ascontiguousarray(colidx, dtype=np.int32)
+    arrs, dtype = _features(Lf, Rf, Rf)
+    Lf, Rf = arrs[0], arrs[1]
+    att = np.ascontiguousarray(att, dtype=np.float32)
+    N, H, D = Lf.shape
+    if att.shape != (H, D):
+        raise ValueError("att must be [H, D]")
+    rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    nrows = N if rows is None else rows_arr.size
+    out = np.empty((nrows, H, D))
+    absagg = np.empty_like(out) if want_absagg else None
+    lse = np.empty((nrows, H)) if want_lse else None
+    rc = _load().gt_oracle_gatv2_fwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Lf), _ptr(Rf),
+                                     _ptr(att), N, colidx.size, H, D, ctypes.c_float(float(slope)),
+                                     _ptr(rows_arr), nrows, _ptr(out), _ptr(absagg), _ptr(lse))
+    if rc:
+        raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
+    return out, absagg, lse

@@ -335,3 +335,83 @@ int gt_oracle_bwd_dkv(int dtype, const int64_t* rowptr, const int32_t* colidx,
     free(need);
     return 0;
 }
+
+/* ------------------------------------------------------------- GATv2
+ *
+ * Forward of the GATv2 attention (paper, Section 2.2, attention family (iii):
+ * e_ij = a^T LeakyReLU(W_l h_i + W_r h_j), values v_j = W_r h_j; Appendix D.2,
+ * "Fused forward in CSR (GATv2)").  With the projected features given,
+ * Lf = W_l h and Rf = W_r h as [N][H][D], and the attention vector att
+ * [H][D] (float32), per row i and head h over the CSR entries e of row i:
+ *     s_e = sum_d att[h,d] * LeakyReLU(Lf[i,h,d] + Rf[j_e,h,d])
+ *     out[i,h,:] = sum_e softmax_e(s) * Rf[j_e,h,:]
+ * with LeakyReLU(x) = x for x > 0, slope * x otherwise.  Same two-pass
+ * softmax, outputs (out, absagg, lse) and conventions as gt_oracle_fwd.
+ */
+int gt_oracle_gatv2_fwd(int dtype, const int64_t* rowptr, const int32_t* colidx, const void* Lf,
+                        const void* Rf, const float* att, int64_t N, int64_t E, int32_t H,
+                        int32_t D, float slope, const int64_t* rows, int64_t nrows, double* out,
+                        double* absagg, double* lse) {
+    if ((dtype != ORACLE_F32 && dtype != ORACLE_BF16) || N < 0 || E < 0 || H < 1 || D < 1 ||
+        nrows < 0 || !rowptr || !att || (nrows > 0 && !out) || (E > 0 && !colidx) ||
+        (N > 0 && (!Lf || !Rf)) || (!rows && nrows != N))
+        return 1;
+    if (rowptr[0] != 0 || rowptr[N] != E) return 2;
+    const double sl = (double)slope;
+    int status = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : status)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows ? rows[r] : r;
+        if (i < 0 || i >= N) { status |= 2; continue; }
+        const int64_t b = rowptr[i], e = rowptr[i + 1];
+        if (b < 0 || e < b || e > E) { status |= 2; continue; }
+        const int64_t deg = e - b;
+        int bad_col = 0;
+        for (int64_t t = 0; t < deg; ++t)
+            if (colidx[b + t] < 0 || colidx[b + t] >= N) bad_col = 1;
+        if (bad_col) { status |= 2; continue; }
+        double* s = (double*)malloc((size_t)(deg > 0 ? deg : 1) * sizeof(double));
+        for (int32_t h = 0; h < H; ++h) {
+            double* o = out + (r * H + h) * (int64_t)D;
+            double* a = absagg ? absagg + (r * H + h) * (int64_t)D : NULL;
+            for (int32_t d = 0; d < D; ++d) {
+                o[d] = 0.0;
+                if (a) a[d] = 0.0;
+            }
+            if (deg == 0) {
+                if (lse) lse[r * H + h] = -INFINITY;
+                continue;
+            }
+            double m = -INFINITY;
+            for (int64_t t = 0; t < deg; ++t) {
+                const int64_t j = colidx[b + t];
+                double acc = 0.0;
+                for (int32_t d = 0; d < D; ++d) {
+                    const double x = elem(Lf, dtype, (i * H + h) * (int64_t)D + d) +
+                                     elem(Rf, dtype, (j * H + h) * (int64_t)D + d);
+                    acc += (double)att[h * D + d] * (x > 0.0 ? x : sl * x);
+                }
+                s[t] = acc;
+                if (s[t] > m) m = s[t];
+            }
+            double Z = 0.0;
+            for (int64_t t = 0; t < deg; ++t) {
+                const int64_t j = colidx[b + t];
+                const double w = exp(s[t] - m);
+                Z += w;
+                for (int32_t d = 0; d < D; ++d) {
+                    const double v = elem(Rf, dtype, (j * H + h) * (int64_t)D + d);
+                    o[d] += w * v;
+                    if (a) a[d] += w * fabs(v);
+                }
+            }
+            for (int32_t d = 0; d < D; ++d) {
+                o[d] /= Z;
+                if (a) a[d] /= Z;
+            }
+            if (lse) lse[r * H + h] = m + log(Z);
+        }
+        free(s);
+    }
+    return status ? 2 : 0;
+}

@@ -34,8 +34,15 @@ MUTANTS = {
     "bwd_dk_without_scale": ("gk[d] += sc * ds * qv;", "gk[d] += ds * qv;"),
     "bwd_dv_without_alpha": ("gv[d] += alpha * go;", "gv[d] += go;"),
     "bwd_dq_sign": ("g[d] += sc * ds * kv;", "g[d] -= sc * ds * kv;"),
+    "gatv2_slope_on_positive": ("(x > 0.0 ? x : sl * x)", "(x > 0.0 ? sl * x : x)"),
+    "gatv2_no_attention_vector": ("acc += (double)att[h * D + d] * (x > 0.0 ? x : sl * x);",
+                                  "acc += (x > 0.0 ? x : sl * x);"),
+    "gatv2_left_as_value": ("const double v = elem(Rf, dtype, (j * H + h) * (int64_t)D + d);",
+                            "const double v = elem(Lf, dtype, (j * H + h) * (int64_t)D + d);"),
+    "gatv2_row_term_from_source": ("const double x = elem(Lf, dtype, (i * H + h) * (int64_t)D + d) +",
+                                   "const double x = elem(Lf, dtype, (j * H + h) * (int64_t)D + d) +"),
 }
-PIN_FILES = ["test_oracle_pins.py", "test_oracle_bwd_pins.py"]
+PIN_FILES = ["test_oracle_pins.py", "test_oracle_bwd_pins.py", "test_oracle_gatv2_pins.py"]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
