@@ -9,7 +9,10 @@ events on the launch stream, and the float64 CPU oracle timed on this host.
 
 Default workload: the power-law graph shaped like ogbn-arxiv (169,343 nodes,
 in-degree ~ shifted Zipf exponent 2.1, 4 heads x 32 dims, fp32 features);
-``--config`` selects one of the five workload shapes by index.
+``--config`` selects one of the five workload shapes by index; ``--gatv2``
+times the GATv2 forward (same skeleton, score a^T LeakyReLU(l_i + r_j), one
+gathered row per entry) on the same graph, with L, R the workload's first two
+feature tensors and a N(0, 1/D) attention vector.
 """
 from __future__ import annotations
 
@@ -22,6 +25,8 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "fused graph-attention fwd GEdges/s at 1 MI355X; achieved HBM GB/s vs peak"
+GATV2_METRIC = "fused GATv2 attention fwd GEdges/s at 1 MI355X; achieved HBM GB/s vs peak"
+GATV2_SLOPE = 0.2
 HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2605_31500_amd", "csrc", "gt_attn.hip")
@@ -34,10 +39,25 @@ def model_bytes(w) -> int:
     return 8 * (w.N + 1) + 4 * w.E + w.N * R + 2 * w.E * R + w.N * R
 
 
-def compulsory_bytes(w) -> int:
+def gatv2_model_bytes(w) -> int:
+    """GATv2: rowptr + colidx + L + R gathered once per CSR entry (score operand
+    and value) + out + the attention vector."""
     eb = 4 if w.dtype == "f32" else 2
     R = w.H * w.D * eb
-    return 8 * (w.N + 1) + 4 * w.E + 4 * w.N * R
+    return 8 * (w.N + 1) + 4 * w.E + w.N * R + w.E * R + w.N * R + 4 * w.H * w.D
+
+
+def gatv2_attention_vector(w, seed: int):
+    import math
+    import synth
+    return synth.normal(seed, synth.STREAM_EXTRA + 9, (w.H, w.D), 1.0 / math.sqrt(w.D), "f32")
+
+
+def compulsory_bytes(w, gatv2: bool = False) -> int:
+    """Each input and output byte once (Q, K, V, out; GATv2: L, R, out)."""
+    eb = 4 if w.dtype == "f32" else 2
+    R = w.H * w.D * eb
+    return 8 * (w.N + 1) + 4 * w.E + (3 if gatv2 else 4) * w.N * R
 
 
 def backward_model_bytes(w) -> int:
@@ -110,12 +130,16 @@ def stored_traffic(workload: str):
     return entry.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, seconds: float) -> dict:
+def cpu_baseline(w, seconds: float, att=None) -> dict:
     import oracle
     passes, t0 = 0, time.perf_counter()
     while True:
-        oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_absagg=False,
-                           want_lse=False)
+        if att is None:
+            oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_absagg=False,
+                               want_lse=False)
+        else:
+            oracle.gatv2_fwd(w.rowptr, w.colidx, w.Q, w.K, att, GATV2_SLOPE, want_absagg=False,
+                             want_lse=False)
         passes += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -151,6 +175,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass (gt_attn_bwd) instead of the forward")
+    ap.add_argument("--gatv2", action="store_true",
+                    help="time the GATv2 forward (gt_gatv2_fwd) on the same graph")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
                     help="enable the matrix-core path for dense 64-id windows holding at "
                          "least MIN in-window entries (bf16, H*D <= 128)")
@@ -183,9 +209,16 @@ def main() -> int:
     stream = torch.cuda.current_stream()
 
     tuning = {"dense_tiles": args.dense_tiles} if args.dense_tiles else None
+    att = gatv2_attention_vector(w, args.config) if args.gatv2 else None
+    if args.gatv2:
+        att_d = to_device(att)
 
-    def step():
-        gt.gt_attn_fwd_ex(*dev, out, w.scale, tuning=tuning, stream=stream)
+        def step():
+            gt.gt_gatv2_fwd(dev[0], dev[1], dev[2], dev[3], att_d, GATV2_SLOPE, out,
+                            tuning=tuning, stream=stream)
+    else:
+        def step():
+            gt.gt_attn_fwd_ex(*dev, out, w.scale, tuning=tuning, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -211,12 +244,12 @@ def main() -> int:
     phase_ms, calls = gt.gt_profile_collect()
     gt.gt_profile_enable(False)
     attn_ms = phase_ms[1] / calls
-    mbytes = model_bytes(w)
+    mbytes = gatv2_model_bytes(w) if args.gatv2 else model_bytes(w)
     achieved = mbytes / (attn_ms * 1e-3) / 1e9
-    traffic = stored_traffic(w.name)
+    traffic = stored_traffic(w.name + (":gatv2" if args.gatv2 else ""))
 
     rec = {
-        "metric": METRIC,
+        "metric": GATV2_METRIC if args.gatv2 else METRIC,
         "value": round(w.E / (ms_per_step * 1e-3) / 1e9, 4),
         "unit": "GEdges/s",
         "n_gpus": 1,
@@ -228,10 +261,11 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": w.dtype,
         "data": "synthetic",
-        "config": dict(w.describe(), **({"dense_tiles": args.dense_tiles} if args.dense_tiles else {})),
+        "config": dict(w.describe(), **({"dense_tiles": args.dense_tiles} if args.dense_tiles else {}),
+                       **({"layer": "gatv2", "slope": GATV2_SLOPE} if args.gatv2 else {})),
         "roofline": {
             "bound": "hbm",
-            "kernel": "gt_attn_kernel",
+            "kernel": "gt_attn_kernel" + (" (GATv2 score)" if args.gatv2 else ""),
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
@@ -243,10 +277,10 @@ def main() -> int:
         "phases_ms": {"partition": round(phase_ms[0] / calls, 5), "attention": round(attn_ms, 5),
                       "merge": round(phase_ms[2] / calls, 5)},
         "whole_call_model_GBps": round(mbytes / (ms_per_step * 1e-3) / 1e9, 1),
-        "compulsory_bytes": compulsory_bytes(w),
+        "compulsory_bytes": compulsory_bytes(w, args.gatv2),
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, att)
     print(json.dumps(rec), flush=True)
     return 0
 

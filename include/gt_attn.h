@@ -144,6 +144,30 @@ gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* c
                          const gt_tuning* tuning, hipStream_t stream);
 
 /*
+ * GATv2 forward (paper Section 2.2, the GATv2 member of the attention family;
+ * Appendix D.2, "Fused forward in CSR (GATv2)"), on the same fused streaming
+ * pass and degree-aware partition as gt_attn_fwd_ex:
+ *
+ *     s_e        = sum_d att[h,d] * LeakyReLU(L[i,h,d] + R[j_e,h,d])
+ *     out[i,h,:] = sum_e softmax_e(s) * R[j_e,h,:]
+ *
+ * with LeakyReLU(x) = x for x > 0, else slope * x.  L and R are the
+ * precomputed per-node features (the two linear maps of the layer applied to
+ * the node states); R gives both the score operand and the value, so each CSR
+ * entry gathers one row.  No logit scaling.  An empty row yields zeros.
+ * Layouts: L, R, out [N][H][D] in `dtype` (16-byte aligned; out must not
+ * overlap L or R); att fp32 [H][D] device memory, 16-byte aligned; lse
+ * (may be NULL) float [N][H], ln(sum_e exp(s_e)), -inf for an empty row.
+ * slope must be finite.  tuning as for gt_attn_fwd_ex, except dense_tiles,
+ * which is ignored.  Same ownership, workspace, asynchrony and error contract
+ * as gt_attn_fwd.
+ */
+gt_status gt_gatv2_fwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const void* L,
+                       const void* R, const float* att, float slope, void* out, float* lse,
+                       int64_t N, int64_t E, int32_t H, int32_t D, const gt_tuning* tuning,
+                       hipStream_t stream);
+
+/*
  * Backward pass (paper Appendix D.2, backward of the graph transformer):
  * gradients dQ, dK, dV of sum(out * dout) for the forward defined above.
  * The attention weights are recomputed from lse, the forward's per-row

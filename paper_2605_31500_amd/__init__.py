@@ -25,7 +25,8 @@ GT_DTYPE_F32 = 0
 GT_DTYPE_BF16 = 1
 
 EXPORTED_SYMBOLS = (
-    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_attn_bwd", "gt_csr_validate", "gt_status_string",
+    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd", "gt_csr_validate",
+    "gt_status_string",
     "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
 )
 
@@ -60,6 +61,8 @@ def load_library(path: str = LIB_PATH):
     L.gt_attn_fwd.argtypes = sig
     L.gt_attn_fwd_bf16.argtypes = sig
     L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:6] + [P] + sig[6:-1] + [ctypes.POINTER(GtTuning), P]
+    L.gt_gatv2_fwd.argtypes = [ctypes.c_int, P, P, P, P, P, f32, P, P, i64, i64, i32, i32,
+                               ctypes.POINTER(GtTuning), P]
     L.gt_attn_bwd.argtypes = [ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, P, i64, i64, i32, i32,
                               f32, P]
     L.gt_csr_validate.argtypes = [P, P, i64, i64, ctypes.POINTER(i32), P]
@@ -70,7 +73,8 @@ def load_library(path: str = LIB_PATH):
     L.gt_profile_enable.argtypes = [i32]
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     L.gt_workspace_release.argtypes = []
-    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_attn_bwd", "gt_csr_validate",
+    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
+                 "gt_csr_validate",
                  "gt_profile_enable", "gt_profile_collect", "gt_workspace_release"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -151,6 +155,31 @@ def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None
     _check(load_library().gt_attn_fwd_ex(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
                                          _ptr(V), _ptr(out), _ptr(lse), N, colidx.numel(), H, D,
                                          float(scale), tp, _stream(Q.device, stream)))
+
+
+def gt_gatv2_fwd(rowptr, colidx, L, R, att, slope, out, tuning=None, stream=None, lse=None) -> None:
+    """GATv2 forward: out[i] = sum_e softmax_e(<att, LeakyReLU(L[i] + R[j_e])>) R[j_e]
+    per head.  L, R, out: [N, H, D] (dtype from L); att: float32 [H, D] device
+    tensor; slope: LeakyReLU negative slope; lse as in gt_attn_fwd_ex."""
+    if L.dtype == torch.float32:
+        dtype, allowed = GT_DTYPE_F32, (torch.float32,)
+    else:
+        dtype, allowed = GT_DTYPE_BF16, (torch.bfloat16, torch.int16, torch.uint16)
+    _check_tensors(rowptr, colidx, L, R, R, out, allowed)
+    N, H, D = L.shape
+    if not (isinstance(att, torch.Tensor) and att.is_cuda and att.is_contiguous()
+            and att.dtype == torch.float32 and tuple(att.shape) == (H, D)):
+        raise ValueError("att must be a contiguous float32 [H, D] device tensor")
+    if isinstance(tuning, dict):
+        tuning = GtTuning(**tuning)
+    tp = ctypes.byref(tuning) if tuning is not None else None
+    if lse is not None:
+        if not (lse.is_cuda and lse.is_contiguous() and lse.dtype == torch.float32
+                and tuple(lse.shape) == (N, H)):
+            raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
+    _check(load_library().gt_gatv2_fwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(L), _ptr(R),
+                                       _ptr(att), float(slope), _ptr(out), _ptr(lse), N,
+                                       colidx.numel(), H, D, tp, _stream(L.device, stream)))
 
 
 def gt_attn_bwd(rowptr, colidx, rowptr_t, colidx_t, Q, K, V, out, dout, lse, dQ, dK, dV, scale,

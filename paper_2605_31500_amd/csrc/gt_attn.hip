@@ -4,6 +4,10 @@
 // logits; single streaming pass with online softmax (Section 3.2, Appendix
 // D.2).  For every destination row i and head h:
 //     out[i,h,:] = sum_e softmax_e(scale * <Q[i,h,:], K[j_e,h,:]>) V[j_e,h,:]
+// The same skeleton evaluates the GATv2 layer of the same family (Section 2.2;
+// Appendix D.2, fused GATv2 forward), selected by the KIND template argument:
+//     out[i,h,:] = sum_e softmax_e(<a[h,:], LeakyReLU(L[i,h,:] + R[j_e,h,:])>) R[j_e,h,:]
+// where each CSR entry gathers one row (R serves as key and value).
 //
 // Mapping (designed for 64-wide wavefronts, not taken from the paper's
 // one-block-per-(node, head) CUDA layout):
@@ -59,6 +63,9 @@ constexpr int kXcds = 8;
 // workspace holds two counter sets used by alternate calls: a call uses one
 // set (zero on entry) and its attention kernel zeroes the other set for the
 // next call, so no reset has to wait for the end of the call.
+// Score kinds of the attention skeleton.
+enum { KIND_GT = 0, KIND_GATV2 = 1 };
+
 enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_COUNT = 4 };
 constexpr int kCntStride = 64;                          // ints between counters
 constexpr int kCntSetWords = CNT_COUNT * kCntStride;   // one counter set
@@ -111,7 +118,9 @@ struct AttnParams {
     char* out;
     float* lse;  // [N][H] natural-log logsumexp of the scaled scores, or nullptr
     int64_t N;
-    float c;  // scale * log2(e)
+    float c;  // scale * log2(e); log2(e) for GATv2
+    const float* att;  // GATv2 attention vector [H][D]
+    float slope;       // GATv2 LeakyReLU negative slope
     int32_t light_max;
     int32_t cap_chunks;
     const int32_t* counters;
@@ -225,20 +234,39 @@ __device__ __forceinline__ float lse_of(float m, float l) {
 
 // ------------------------------------------------------------ per-lane state
 
-template <typename T, int H, int D>
+// One lane's share of a row's running state.  KIND_GT: q holds Q[i] and each
+// entry loads K[j] (score) and V[j] (value).  KIND_GATV2: q holds L[i], a the
+// lane's slice of the attention vector, and each entry loads only R[j], which
+// gives both the score and the value.
+template <typename T, int H, int D, int KIND = KIND_GT>
 struct RowState {
     using Gm = Geo<T, H, D>;
+    static constexpr bool kGat = KIND == KIND_GATV2;
     float q[Gm::kNV][Gm::kEPV];
+    float a[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
     float acc[Gm::kNV][Gm::kEPV];
     float m[Gm::kNV];  // running max of log2-scaled scores for this lane's head
     float l[Gm::kNV];  // running sum of 2^(s - m)
 
-    __device__ __forceinline__ void begin(const char* __restrict__ Qb, int64_t row, int lig) {
+    __device__ __forceinline__ void begin(const char* __restrict__ Qb, int64_t row, int lig,
+                                          const float* __restrict__ att = nullptr) {
         const char* qrow = Qb + row * (int64_t)Gm::kRowBytes + lig * 16;
 #pragma unroll
         for (int k = 0; k < Gm::kNV; ++k) {
             const uint4 r = *reinterpret_cast<const uint4*>(qrow + k * Gm::kG * 16);
             widen<T>(r, q[k]);
+            if constexpr (kGat) {
+                // the attention vector is [H][D] fp32 in the row's element order
+                const float* av = att + (lig + k * Gm::kG) * Gm::kEPV;
+#pragma unroll
+                for (int e = 0; e < Gm::kEPV; e += 4) {
+                    const float4 x = *reinterpret_cast<const float4*>(av + e);
+                    a[k][e] = x.x;
+                    a[k][e + 1] = x.y;
+                    a[k][e + 2] = x.z;
+                    a[k][e + 3] = x.w;
+                }
+            }
             m[k] = -INFINITY;
             l[k] = 0.0f;
 #pragma unroll
@@ -246,10 +274,11 @@ struct RowState {
         }
     }
 
-    // Loads of one step: the K and V rows of U entries, 16 bytes per lane each.
+    // Loads of one step: the K and V rows (GATv2: the R rows) of U entries,
+    // 16 bytes per lane each.
     struct Batch {
         uint4 k[Gm::kU][Gm::kNV];
-        uint4 v[Gm::kU][Gm::kNV];
+        uint4 v[kGat ? 1 : Gm::kU][Gm::kNV];
     };
 
     __device__ __forceinline__ void issue(const char* __restrict__ Kb, const char* __restrict__ Vb,
@@ -260,14 +289,15 @@ struct RowState {
 #pragma unroll
             for (int k = 0; k < Gm::kNV; ++k) {
                 bt.k[u][k] = *reinterpret_cast<const uint4*>(Kb + off + k * Gm::kG * 16);
-                bt.v[u][k] = *reinterpret_cast<const uint4*>(Vb + off + k * Gm::kG * 16);
+                if constexpr (!kGat) bt.v[u][k] = *reinterpret_cast<const uint4*>(Vb + off + k * Gm::kG * 16);
             }
         }
     }
 
     // Online-softmax update with the U entries of a batch; entries u >= nvalid
     // are copies of valid indices and contribute nothing (score -inf).
-    __device__ __forceinline__ void consume(const Batch& bt, int nvalid, float c) {
+    // slope is the GATv2 LeakyReLU slope (unused for the dot-product score).
+    __device__ __forceinline__ void consume(const Batch& bt, int nvalid, float c, float slope = 0.0f) {
         // No implicit contraction: fusing the score product into the later
         // subtraction of the running max would give the maximal entry a weight
         // of 2^(rounding error) instead of exactly 1.
@@ -281,8 +311,16 @@ struct RowState {
                 float kf[Gm::kEPV];
                 widen<T>(bt.k[u][k], kf);
                 float d = 0.0f;
+                if constexpr (kGat) {
 #pragma unroll
-                for (int e = 0; e < Gm::kEPV; ++e) d = fmaf(q[k][e], kf[e], d);
+                    for (int e = 0; e < Gm::kEPV; ++e) {
+                        const float x = q[k][e] + kf[e];
+                        d = fmaf(a[k][e], x > 0.0f ? x : slope * x, d);
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < Gm::kEPV; ++e) d = fmaf(q[k][e], kf[e], d);
+                }
                 d = head_sum<Gm::kHL>(d) * c;
                 s[u][k] = (u < nvalid) ? d : -INFINITY;
             }
@@ -301,7 +339,10 @@ struct RowState {
                 const float pu = fast_exp2(s[u][k] - mb);
                 l[k] += pu;
                 float vf[Gm::kEPV];
-                widen<T>(bt.v[u][k], vf);
+                if constexpr (kGat)
+                    widen<T>(bt.k[u][k], vf);
+                else
+                    widen<T>(bt.v[u][k], vf);
 #pragma unroll
                 for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = fmaf(pu, vf[e], acc[k][e]);
             }
@@ -310,10 +351,11 @@ struct RowState {
     }
 
     __device__ __forceinline__ void step(const char* __restrict__ Kb, const char* __restrict__ Vb,
-                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c) {
+                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c,
+                                         float slope = 0.0f) {
         Batch bt;
         issue(Kb, Vb, j, lig, bt);
-        consume(bt, nvalid, c);
+        consume(bt, nvalid, c, slope);
     }
 
     // Merge the state held by the lane `off` positions away (same vector
@@ -369,14 +411,14 @@ struct RowState {
 
 // One wavefront streams CSR entries [b, e) of `row`; slot < 0 writes the
 // normalised output, slot >= 0 writes the partial state of a chunk.
-template <typename T, int H, int D>
+template <typename T, int H, int D, int KIND>
 __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, int64_t b, int64_t e,
                                              int32_t slot, int32_t* __restrict__ tile, int lane) {
     using Gm = Geo<T, H, D>;
     constexpr int U = Gm::kU, P = Gm::kP, G = Gm::kG;
     const int g = lane / G, lig = lane % G;
-    RowState<T, H, D> st;
-    st.begin(p.Q, row, lig);
+    RowState<T, H, D, KIND> st;
+    st.begin(p.Q, row, lig, p.att);
     for (int64_t tb = b; tb < e; tb += kWave) {
         const int64_t pos = (tb + lane < e) ? tb + lane : e - 1;
         const int32_t idx = p.colidx[pos];
@@ -391,7 +433,7 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
                 int32_t j[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) j[u] = tile[e0 + u];
-                st.step(p.K, p.V, j, nvalid, lig, p.c);
+                st.step(p.K, p.V, j, nvalid, lig, p.c, p.slope);
             }
         }
     }
@@ -410,7 +452,7 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
 // loaded before the current row's work starts, and its first index tile is
 // loaded while the current row's first K/V batch is in flight, so a short row
 // costs about one memory latency instead of three (rowptr -> colidx -> K/V).
-template <typename T, int H, int D>
+template <typename T, int H, int D, int KIND>
 __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int64_t it_end,
                                            int64_t stride, int g, int lig,
                                            int32_t* __restrict__ gtile) {
@@ -433,8 +475,8 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
         mine = ok && (e - b) <= p.light_max;
         bool fetched = false;
         if (cmine) {
-            RowState<T, H, D> st;
-            st.begin(p.Q, crow, lig);
+            RowState<T, H, D, KIND> st;
+            st.begin(p.Q, crow, lig, p.att);
             for (int64_t tb = cb; tb < ce; tb += G) {
                 int32_t tile_idx = cidx;
                 if (tb != cb) tile_idx = p.colidx[(tb + lig < ce) ? tb + lig : ce - 1];
@@ -447,13 +489,13 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
                     int32_t j[U];
 #pragma unroll
                     for (int u = 0; u < U; ++u) j[u] = gtile[t + u];
-                    typename RowState<T, H, D>::Batch bt;
+                    typename RowState<T, H, D, KIND>::Batch bt;
                     st.issue(p.K, p.V, j, lig, bt);
                     if (!fetched) {  // next row's first tile, overlapped with this batch
                         idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
                         fetched = true;
                     }
-                    st.consume(bt, nvalid, p.c);
+                    st.consume(bt, nvalid, p.c, p.slope);
                 }
             }
             st.store_out(p.out, p.lse, crow, lig);
@@ -465,7 +507,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
 // Attention kernel: first the chunk items (pieces of heavy rows,
 // then whole medium rows), one wavefront each; then the light rows, P per
 // wavefront, in XCD-contiguous ranges.
-template <typename T, int H, int D>
+template <typename T, int H, int D, int KIND>
 __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     using Gm = Geo<T, H, D>;
     __shared__ int32_t tiles[kWavesPerBlock][kWave];
@@ -482,10 +524,10 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     for (int it = blockIdx.x * kWavesPerBlock + wv; it < n_items; it += nwaves) {
         if (it < n_chunks) {
             const ChunkItem ci = p.chunks[it];
-            wave_segment<T, H, D>(p, ci.row, ci.begin, ci.end, ci.slot, tile, lane);
+            wave_segment<T, H, D, KIND>(p, ci.row, ci.begin, ci.end, ci.slot, tile, lane);
         } else {
             const int64_t row = p.med_list[it - n_chunks];
-            wave_segment<T, H, D>(p, row, p.rowptr[row], p.rowptr[row + 1], -1, tile, lane);
+            wave_segment<T, H, D, KIND>(p, row, p.rowptr[row], p.rowptr[row + 1], -1, tile, lane);
         }
     }
 
@@ -495,7 +537,7 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
     const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
     const int g = lane / Gm::kG, lig = lane % Gm::kG;
-    if (!p.skip_light) light_rows<T, H, D>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * Gm::kG);
+    if (!p.skip_light) light_rows<T, H, D, KIND>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * Gm::kG);
 }
 
 // ------------------------------------------------------- dense-tile path
@@ -1083,6 +1125,9 @@ struct Args {
     int64_t N, E;
     int32_t H, D;
     float scale;
+    int kind = KIND_GT;
+    const float* att = nullptr;  // GATv2 attention vector
+    float slope = 0.0f;          // GATv2 LeakyReLU slope
 };
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -1098,20 +1143,21 @@ int device_cus(int dev) {
     return cache[dev];
 }
 
-template <typename T, int H, int D>
+template <typename T, int H, int D, int KIND>
 int attn_blocks_per_cu(int dev) {
     static int cache[64] = {0};
     if (dev < 0 || dev >= 64) return 4;
     if (cache[dev] == 0) {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, gt_attn_kernel<T, H, D>, kBlock, 0) != hipSuccess || nb <= 0)
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, gt_attn_kernel<T, H, D, KIND>, kBlock, 0) != hipSuccess ||
+            nb <= 0)
             nb = 4;
         cache[dev] = nb;
     }
     return cache[dev];
 }
 
-template <typename T, int H, int D>
+template <typename T, int H, int D, int KIND>
 gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
     // Defaults chosen by measurement on the five workload shapes (power law,
@@ -1130,7 +1176,8 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
         if (tu->grid_blocks > 0) grid = tu->grid_blocks;
     }
     if (heavy_min <= light_max) heavy_min = light_max + 1;
-    constexpr bool kTileShape = std::is_same<T, bf16_tag>::value && H * D <= 128 && D % 32 == 0;
+    constexpr bool kTileShape =
+        KIND == KIND_GT && std::is_same<T, bf16_tag>::value && H * D <= 128 && D % 32 == 0;
     const bool tiles = kTileShape && tile_min > 0;
     if (tiles && light_max > kWinMaxDeg) light_max = kWinMaxDeg;
 
@@ -1139,14 +1186,14 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
     if (grid <= 0 && tiles) {
         // light rows belong to the tile kernel: only the wave items remain
-        grid = 4 * device_cus(dev) * attn_blocks_per_cu<T, H, D>(dev);
+        grid = 4 * device_cus(dev) * attn_blocks_per_cu<T, H, D, KIND>(dev);
     }
     if (grid <= 0) {
         // About two light items (P rows each) per wave, between 4x and 64x the
         // number of workgroups the device holds at once: finer than one
         // resident wave of workgroups so the hardware scheduler evens out the
         // per-wave work, coarse enough to keep dispatch cheap.
-        const int64_t resident = (int64_t)device_cus(dev) * attn_blocks_per_cu<T, H, D>(dev);
+        const int64_t resident = (int64_t)device_cus(dev) * attn_blocks_per_cu<T, H, D, KIND>(dev);
         const int64_t light_items = (a.N + Gm::kP - 1) / Gm::kP;
         int64_t g = light_items / (2 * kWavesPerBlock);
         if (g < 4 * resident) g = 4 * resident;
@@ -1255,7 +1302,9 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.out = static_cast<char*>(a.out);
     ap.lse = a.lse;
     ap.N = a.N;
-    ap.c = a.scale * 1.4426950408889634f;
+    ap.c = (KIND == KIND_GT ? a.scale : 1.0f) * 1.4426950408889634f;
+    ap.att = a.att;
+    ap.slope = a.slope;
     ap.light_max = light_max;
     ap.cap_chunks = (int32_t)cap_chunks;
     ap.counters = counters;
@@ -1265,7 +1314,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
     ap.part_ml = reinterpret_cast<float2*>(ws + o_ml);
     ap.skip_light = tiles ? 1 : 0;
-    hipLaunchKernelGGL((gt_attn_kernel<T, H, D>), dim3(grid), dim3(kBlock), 0, stream, ap);
+    hipLaunchKernelGGL((gt_attn_kernel<T, H, D, KIND>), dim3(grid), dim3(kBlock), 0, stream, ap);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "attention launch");
     if (prof) (void)hipEventRecord(ev[2], stream);
 
@@ -1295,10 +1344,10 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
 
 using LaunchFn = gt_status (*)(const Args&, const gt_tuning*, hipStream_t);
 
-template <typename T>
+template <typename T, int KIND>
 LaunchFn pick_hd(int32_t H, int32_t D) {
 #define GT_CASE(h, d) \
-    if (H == h && D == d) return &launch<T, h, d>;
+    if (H == h && D == d) return &launch<T, h, d, KIND>;
     GT_CASE(1, 32) GT_CASE(1, 64) GT_CASE(1, 128)
     GT_CASE(2, 32) GT_CASE(2, 64) GT_CASE(2, 128)
     GT_CASE(4, 32) GT_CASE(4, 64) GT_CASE(4, 128)
@@ -1319,25 +1368,37 @@ gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t st
     if (a.E < 0 || a.E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
     if (a.H < 1 || a.D < 1) return fail(GT_ERROR_INVALID_VALUE, "H and D must be positive");
     if (!std::isfinite(a.scale)) return fail(GT_ERROR_INVALID_VALUE, "scale must be finite");
-    LaunchFn fn = dtype == GT_DTYPE_F32 ? pick_hd<float>(a.H, a.D) : pick_hd<bf16_tag>(a.H, a.D);
+    if (a.kind == KIND_GATV2 && !std::isfinite(a.slope)) return fail(GT_ERROR_INVALID_VALUE, "slope must be finite");
+    LaunchFn fn;
+    if (a.kind == KIND_GATV2)
+        fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GATV2>(a.H, a.D) : pick_hd<bf16_tag, KIND_GATV2>(a.H, a.D);
+    else
+        fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GT>(a.H, a.D) : pick_hd<bf16_tag, KIND_GT>(a.H, a.D);
     if (!fn)
         return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +
                                                 std::to_string(a.D) + "); H in {1,2,4,8}, D in {32,64,128}");
     if (a.N == 0) return GT_SUCCESS;
     if (!a.rowptr) return fail(GT_ERROR_INVALID_VALUE, "rowptr is null");
     if (a.E > 0 && !a.colidx) return fail(GT_ERROR_INVALID_VALUE, "colidx is null");
-    if (!a.Q || !a.K || !a.V || !a.out) return fail(GT_ERROR_INVALID_VALUE, "Q, K, V and out must be non-null");
+    if (!a.Q || !a.K || !a.V || !a.out) return fail(GT_ERROR_INVALID_VALUE, "Q, K, V and out (L, R and out) must be non-null");
     for (const void* ptr : {a.Q, a.K, a.V, static_cast<const void*>(a.out)})
         if (reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
-            return fail(GT_ERROR_INVALID_VALUE, "Q, K, V and out must be 16-byte aligned");
+            return fail(GT_ERROR_INVALID_VALUE, "Q, K, V and out (L, R and out) must be 16-byte aligned");
     const size_t bytes = (size_t)a.N * a.H * a.D * (dtype == GT_DTYPE_F32 ? 4 : 2);
     for (const void* in : {a.Q, a.K, a.V})
-        if (overlaps(a.out, bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "out overlaps Q, K or V");
+        if (overlaps(a.out, bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "out overlaps Q, K or V (L or R)");
     if (a.lse) {
         const size_t lb = (size_t)a.N * a.H * sizeof(float);
         if (reinterpret_cast<uintptr_t>(a.lse) % 4 != 0) return fail(GT_ERROR_INVALID_VALUE, "lse must be 4-byte aligned");
         for (const void* o : {a.Q, a.K, a.V, static_cast<const void*>(a.out)})
             if (overlaps(a.lse, lb, o, bytes)) return fail(GT_ERROR_INVALID_VALUE, "lse overlaps Q, K, V or out");
+    }
+    if (a.kind == KIND_GATV2) {
+        const size_t ab = (size_t)a.H * a.D * sizeof(float);
+        if (!a.att || reinterpret_cast<uintptr_t>(a.att) % 16 != 0)
+            return fail(GT_ERROR_INVALID_VALUE, "att must be non-null and 16-byte aligned");
+        if (overlaps(a.out, bytes, a.att, ab) || (a.lse && overlaps(a.lse, (size_t)a.N * a.H * sizeof(float), a.att, ab)))
+            return fail(GT_ERROR_INVALID_VALUE, "out or lse overlaps att");
     }
     return fn(a, tu, stream);
 }
@@ -1400,6 +1461,16 @@ gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* c
                          const void* K, const void* V, void* out, float* lse, int64_t N, int64_t E, int32_t H,
                          int32_t D, float scale, const gt_tuning* tuning, hipStream_t stream) {
     return run(dtype, Args{rowptr, colidx, Q, K, V, out, lse, N, E, H, D, scale}, tuning, stream);
+}
+
+gt_status gt_gatv2_fwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const void* L, const void* R,
+                       const float* att, float slope, void* out, float* lse, int64_t N, int64_t E, int32_t H,
+                       int32_t D, const gt_tuning* tuning, hipStream_t stream) {
+    Args a{rowptr, colidx, L, R, R, out, lse, N, E, H, D, 1.0f};
+    a.kind = KIND_GATV2;
+    a.att = att;
+    a.slope = slope;
+    return run(dtype, a, tuning, stream);
 }
 
 gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const int64_t* rowptr_t,

@@ -86,3 +86,29 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError):
         gt.gt_attn_fwd(torch.zeros(4, dtype=torch.int64), torch.zeros(0, dtype=torch.int32), z, z,
                        z, z, 0.1)
+
+
+def call_gatv2(lib, dtype=0, rowptr=FAKE, colidx=FAKE, L=FAKE, R=FAKE + 0x100000,
+               att=FAKE + 0x500000, slope=0.2, out=FAKE + 0x300000, lse=None, N=10, E=20, H=4,
+               D=32):
+    P = ctypes.c_void_p
+    return lib.gt_gatv2_fwd(dtype, P(rowptr), P(colidx), P(L), P(R), P(att),
+                            ctypes.c_float(slope), P(out), P(lse), N, E, H, D, None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=3), 2), (dict(D=16), 2), (dict(dtype=5), 2), (dict(N=-2), 1),
+    (dict(att=0), 1),                           # null attention vector
+    (dict(att=FAKE + 0x500004), 1),             # att misaligned
+    (dict(slope=float("inf")), 1), (dict(slope=float("nan")), 1),
+    (dict(att=FAKE + 0x300000 + 512), 1),       # att overlaps out
+    (dict(L=0), 1), (dict(R=FAKE + 4), 1),
+    (dict(out=FAKE + 0x100000), 1),             # out aliases R
+])
+def test_gatv2_host_validation(lib, kw, status):
+    assert call_gatv2(lib, **kw) == status
+    assert lib.gt_last_error_message()
+
+
+def test_gatv2_empty_graph_is_a_no_op(lib):
+    assert call_gatv2(lib, N=0, E=0) == 0
