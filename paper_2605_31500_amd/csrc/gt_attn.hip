@@ -235,21 +235,25 @@ __device__ __forceinline__ float lse_of(float m, float l) {
 // ------------------------------------------------------------ per-lane state
 
 // One lane's share of a row's running state.  KIND_GT: q holds Q[i] and each
-// entry loads K[j] (score) and V[j] (value).  KIND_GATV2: q holds L[i], a the
-// lane's slice of the attention vector, and each entry loads only R[j], which
-// gives both the score and the value.
+// entry loads K[j] (score) and V[j] (value).  KIND_GATV2: q holds L[i] and each
+// entry loads only R[j], which gives both the score and the value.  The
+// LeakyReLU term uses a * LeakyReLU(x) = a(1+s)/2 * x + a(1-s)/2 * |x| (exact
+// for any slope s): a holds the lane's slice of a(1+s)/2 and a2 of a(1-s)/2,
+// so an element costs one add and two FMAs (|x| is a free operand modifier)
+// instead of a compare, a select and a multiply more.
 template <typename T, int H, int D, int KIND = KIND_GT>
 struct RowState {
     using Gm = Geo<T, H, D>;
     static constexpr bool kGat = KIND == KIND_GATV2;
     float q[Gm::kNV][Gm::kEPV];
     float a[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
+    float a2[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
     float acc[Gm::kNV][Gm::kEPV];
     float m[Gm::kNV];  // running max of log2-scaled scores for this lane's head
     float l[Gm::kNV];  // running sum of 2^(s - m)
 
     __device__ __forceinline__ void begin(const char* __restrict__ Qb, int64_t row, int lig,
-                                          const float* __restrict__ att = nullptr) {
+                                          const float* __restrict__ att = nullptr, float slope = 0.0f) {
         const char* qrow = Qb + row * (int64_t)Gm::kRowBytes + lig * 16;
 #pragma unroll
         for (int k = 0; k < Gm::kNV; ++k) {
@@ -258,13 +262,16 @@ struct RowState {
             if constexpr (kGat) {
                 // the attention vector is [H][D] fp32 in the row's element order
                 const float* av = att + (lig + k * Gm::kG) * Gm::kEPV;
+                const float hs = 0.5f * slope;
 #pragma unroll
                 for (int e = 0; e < Gm::kEPV; e += 4) {
-                    const float4 x = *reinterpret_cast<const float4*>(av + e);
-                    a[k][e] = x.x;
-                    a[k][e + 1] = x.y;
-                    a[k][e + 2] = x.z;
-                    a[k][e + 3] = x.w;
+                    const float4 x4 = *reinterpret_cast<const float4*>(av + e);
+                    const float x[4] = {x4.x, x4.y, x4.z, x4.w};
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        a[k][e + t] = fmaf(hs, x[t], 0.5f * x[t]);
+                        a2[k][e + t] = fmaf(-hs, x[t], 0.5f * x[t]);
+                    }
                 }
             }
             m[k] = -INFINITY;
@@ -296,8 +303,7 @@ struct RowState {
 
     // Online-softmax update with the U entries of a batch; entries u >= nvalid
     // are copies of valid indices and contribute nothing (score -inf).
-    // slope is the GATv2 LeakyReLU slope (unused for the dot-product score).
-    __device__ __forceinline__ void consume(const Batch& bt, int nvalid, float c, float slope = 0.0f) {
+    __device__ __forceinline__ void consume(const Batch& bt, int nvalid, float c) {
         // No implicit contraction: fusing the score product into the later
         // subtraction of the running max would give the maximal entry a weight
         // of 2^(rounding error) instead of exactly 1.
@@ -315,7 +321,8 @@ struct RowState {
 #pragma unroll
                     for (int e = 0; e < Gm::kEPV; ++e) {
                         const float x = q[k][e] + kf[e];
-                        d = fmaf(a[k][e], x > 0.0f ? x : slope * x, d);
+                        d = fmaf(a[k][e], x, d);
+                        d = fmaf(a2[k][e], fabsf(x), d);
                     }
                 } else {
 #pragma unroll
@@ -351,11 +358,10 @@ struct RowState {
     }
 
     __device__ __forceinline__ void step(const char* __restrict__ Kb, const char* __restrict__ Vb,
-                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c,
-                                         float slope = 0.0f) {
+                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c) {
         Batch bt;
         issue(Kb, Vb, j, lig, bt);
-        consume(bt, nvalid, c, slope);
+        consume(bt, nvalid, c);
     }
 
     // Merge the state held by the lane `off` positions away (same vector
@@ -418,7 +424,7 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
     constexpr int U = Gm::kU, P = Gm::kP, G = Gm::kG;
     const int g = lane / G, lig = lane % G;
     RowState<T, H, D, KIND> st;
-    st.begin(p.Q, row, lig, p.att);
+    st.begin(p.Q, row, lig, p.att, p.slope);
     for (int64_t tb = b; tb < e; tb += kWave) {
         const int64_t pos = (tb + lane < e) ? tb + lane : e - 1;
         const int32_t idx = p.colidx[pos];
@@ -433,7 +439,7 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
                 int32_t j[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) j[u] = tile[e0 + u];
-                st.step(p.K, p.V, j, nvalid, lig, p.c, p.slope);
+                st.step(p.K, p.V, j, nvalid, lig, p.c);
             }
         }
     }
@@ -476,7 +482,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
         bool fetched = false;
         if (cmine) {
             RowState<T, H, D, KIND> st;
-            st.begin(p.Q, crow, lig, p.att);
+            st.begin(p.Q, crow, lig, p.att, p.slope);
             for (int64_t tb = cb; tb < ce; tb += G) {
                 int32_t tile_idx = cidx;
                 if (tb != cb) tile_idx = p.colidx[(tb + lig < ce) ? tb + lig : ce - 1];
@@ -495,7 +501,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
                         idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
                         fetched = true;
                     }
-                    st.consume(bt, nvalid, p.c, p.slope);
+                    st.consume(bt, nvalid, p.c);
                 }
             }
             st.store_out(p.out, p.lse, crow, lig);
