@@ -1,13 +1,15 @@
-"""CPU oracle for graph-transformer attention over a CSR graph (float64).
+"""CPU oracle for the CSR operators of the paper: graph-transformer attention
+(forward and backward) and GATv2 attention in float64, and the segment min/max
+reduction with its selected sources.
 
 TEST INFRASTRUCTURE: only ``tests/``, ``__graft_entry__.smoke()`` and the
 CPU-baseline leg of ``bench.py`` may import this package.  The product path
 (the HIP library and its binding) never imports or calls it, and this package
 never imports the product path.
 
-The arithmetic lives in ``gt_oracle.c`` (plain two-pass softmax, per row and
-head, paper Section 2.2 family (iii) with graph-transformer logits).  This
-file only compiles it and marshals numpy arrays.
+The arithmetic lives in ``gt_oracle.c`` (plain two-pass softmax per row and
+head, paper Section 2.2 family (iii); plain per-feature scans for family
+(ii)).  This file only compiles it and marshals numpy arrays.
 """
 from __future__ import annotations
 
@@ -53,6 +55,9 @@ def _load():
         L.gt_oracle_gatv2_fwd.argtypes = [ctypes.c_int, P, P, P, P, P, i64, i64, i32, i32,
                                           ctypes.c_float, P, i64, P, P, P]
         L.gt_oracle_gatv2_fwd.restype = ctypes.c_int
+        L.gt_oracle_segment_reduce.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, i64, i64, i32,
+                                               P, i64, P, P]
+        L.gt_oracle_segment_reduce.restype = ctypes.c_int
         L.gt_oracle_threads.argtypes = []
         L.gt_oracle_threads.restype = ctypes.c_int
         _lib = L
@@ -174,3 +179,37 @@ def gatv2_fwd(rowptr, colidx, Lf, Rf, att, slope, rows=None, want_absagg=True, w
     if rc:
         raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
     return out, absagg, lse
+
+
+REDUCE_OPS = {"min": 0, "max": 1}
+
+
+def segment_reduce(rowptr, colidx, X, op="min", rows=None):
+    """Min or max of each row's source features (paper Section 2.2, family (ii)),
+    with the source that attains it.  X: [N, F] float32 or uint16 bf16 bits.
+    Returns (out float32 [nrows, F], arg int32 [nrows, F]); an empty row gives
+    0 and -1.  Ties go to the smallest source id; -0 orders below +0."""
+    rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
+    colidx = np.ascontiguousarray(colidx, dtype=np.int32)
+    X = np.ascontiguousarray(X)
+    if X.dtype == np.float32:
+        dtype = 0
+    elif X.dtype == np.uint16:
+        dtype = 1
+    else:
+        raise TypeError("X must be float32 or uint16 (bf16 bits)")
+    if X.ndim != 2:
+        raise ValueError("X must be [N, F]")
+    N, F = X.shape
+    if rowptr.size != N + 1:
+        raise ValueError("rowptr must have N+1 entries")
+    rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    nrows = N if rows is None else rows_arr.size
+    out = np.empty((nrows, F), dtype=np.float32)
+    arg = np.empty((nrows, F), dtype=np.int32)
+    rc = _load().gt_oracle_segment_reduce(dtype, REDUCE_OPS[op], _ptr(rowptr), _ptr(colidx),
+                                          _ptr(X), N, colidx.size, F, _ptr(rows_arr), nrows,
+                                          _ptr(out), _ptr(arg))
+    if rc:
+        raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
+    return out, arg

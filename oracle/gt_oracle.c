@@ -1,5 +1,7 @@
 /*
- * CPU oracle: graph-transformer attention over a CSR graph, in float64.
+ * CPU oracle: graph-transformer attention over a CSR graph, in float64 (this
+ * header); its backward, the GATv2 forward and the segment min/max reduction
+ * follow further down, each with its own definition.
  *
  * TEST INFRASTRUCTURE.  Only the test suite, the smoke check and the CPU
  * baseline leg of the benchmark may load or call this code.  It shares no
@@ -412,6 +414,82 @@ int gt_oracle_gatv2_fwd(int dtype, const int64_t* rowptr, const int32_t* colidx,
             if (lse) lse[r * H + h] = m + log(Z);
         }
         free(s);
+    }
+    return status ? 2 : 0;
+}
+
+/*
+ * Reduction family (paper Section 2.2, family (ii): h_i <- REDUCE over the
+ * sources j of row i of h_j, REDUCE = min or max; Appendix, degree-aware
+ * reduction-based aggregation: per feature, the reduced value and the source
+ * node that attains it, kept for the backward scatter).
+ *
+ *   out[i,f] = the value X[j_e,f] selected over the CSR entries e of row i
+ *   arg[i,f] = the source j_e it was taken from
+ *
+ * Order (Appendix, order-preserving packing): a value is compared through the
+ * 32-bit key formed from its fp32 bit pattern -- all bits inverted when the
+ * sign bit is set, the sign bit set otherwise -- as an unsigned integer; that
+ * key is then paired with the source index and pairs compare
+ * lexicographically.  So every non-NaN value is ordered as the reals, -0 lies
+ * below +0, and among equal values the smallest source index wins.
+ *   op 0 (min): the entry with the smallest (key, source) pair;
+ *   op 1 (max): the entry with the largest key, ties to the smallest source.
+ * A row with no entries gives out = 0 and arg = -1.  Values are selected,
+ * never computed, so out holds an input value exactly (as fp32; bf16 inputs
+ * are widened exactly).
+ */
+static uint32_t order_key(float x) {
+    uint32_t b;
+    memcpy(&b, &x, sizeof b);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+int gt_oracle_segment_reduce(int dtype, int op, const int64_t* rowptr, const int32_t* colidx,
+                             const void* X, int64_t N, int64_t E, int32_t F,
+                             const int64_t* rows, int64_t nrows, float* out, int32_t* arg) {
+    if ((dtype != ORACLE_F32 && dtype != ORACLE_BF16) || (op != 0 && op != 1) || N < 0 ||
+        E < 0 || F < 1 || nrows < 0 || !rowptr || (nrows > 0 && (!out || !arg)) ||
+        (E > 0 && !colidx) || (N > 0 && !X) || (!rows && nrows != N))
+        return 1;
+    if (rowptr[0] != 0 || rowptr[N] != E) return 2;
+    int status = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : status)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows ? rows[r] : r;
+        if (i < 0 || i >= N) { status |= 2; continue; }
+        const int64_t b = rowptr[i], e = rowptr[i + 1];
+        if (b < 0 || e < b || e > E) { status |= 2; continue; }
+        int bad_col = 0;
+        for (int64_t t = b; t < e; ++t)
+            if (colidx[t] < 0 || colidx[t] >= N) bad_col = 1;
+        if (bad_col) { status |= 2; continue; }
+        for (int32_t f = 0; f < F; ++f) {
+            int have = 0;
+            float best = 0.0f;
+            uint32_t best_key = 0;
+            int32_t best_j = -1;
+            for (int64_t t = b; t < e; ++t) {
+                const int32_t j = colidx[t];
+                const float x = (float)elem(X, dtype, (int64_t)j * F + f);
+                const uint32_t k = order_key(x);
+                int better;
+                if (!have)
+                    better = 1;
+                else if (op == 0)
+                    better = k < best_key || (k == best_key && j < best_j);
+                else
+                    better = k > best_key || (k == best_key && j < best_j);
+                if (better) {
+                    have = 1;
+                    best = x;
+                    best_key = k;
+                    best_j = j;
+                }
+            }
+            out[r * F + f] = have ? best : 0.0f;
+            arg[r * F + f] = have ? best_j : -1;
+        }
     }
     return status ? 2 : 0;
 }

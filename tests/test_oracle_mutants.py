@@ -41,8 +41,21 @@ MUTANTS = {
                             "const double v = elem(Lf, dtype, (j * H + h) * (int64_t)D + d);"),
     "gatv2_row_term_from_source": ("const double x = elem(Lf, dtype, (i * H + h) * (int64_t)D + d) +",
                                    "const double x = elem(Lf, dtype, (j * H + h) * (int64_t)D + d) +"),
+    "reduce_tie_to_largest_source": ("better = k < best_key || (k == best_key && j < best_j);",
+                                     "better = k < best_key || (k == best_key && j > best_j);"),
+    "reduce_key_without_inversion": ("return (b & 0x80000000u) ? ~b : (b | 0x80000000u);",
+                                     "return b | 0x80000000u;"),
+    "reduce_key_ignores_sign_bit": ("return (b & 0x80000000u) ? ~b : (b | 0x80000000u);",
+                                    "return b ^ 0x80000000u;"),
+    "reduce_max_tie_to_largest": ("better = k > best_key || (k == best_key && j < best_j);",
+                                  "better = k >= best_key;"),
+    "reduce_empty_arg_zero": ("arg[r * F + f] = have ? best_j : -1;",
+                              "arg[r * F + f] = have ? best_j : 0;"),
+    "reduce_wrong_feature": ("const float x = (float)elem(X, dtype, (int64_t)j * F + f);",
+                             "const float x = (float)elem(X, dtype, (int64_t)j * F);"),
 }
-PIN_FILES = ["test_oracle_pins.py", "test_oracle_bwd_pins.py", "test_oracle_gatv2_pins.py"]
+PIN_FILES = ["test_oracle_pins.py", "test_oracle_bwd_pins.py", "test_oracle_gatv2_pins.py",
+             "test_oracle_reduce_pins.py"]
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
