@@ -12,7 +12,9 @@ in-degree ~ shifted Zipf exponent 2.1, 4 heads x 32 dims, fp32 features);
 ``--config`` selects one of the five workload shapes by index; ``--gatv2``
 times the GATv2 forward (same skeleton, score a^T LeakyReLU(l_i + r_j), one
 gathered row per entry) on the same graph, with L, R the workload's first two
-feature tensors and a N(0, 1/D) attention vector.
+feature tensors and a N(0, 1/D) attention vector; ``--reduce min|max`` times
+the segment min/max aggregation with its selected sources over the same graph
+with ``--features`` (default 512) fp32 N(0,1) features per node.
 """
 from __future__ import annotations
 
@@ -27,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "fused graph-attention fwd GEdges/s at 1 MI355X; achieved HBM GB/s vs peak"
 GATV2_METRIC = "fused GATv2 attention fwd GEdges/s at 1 MI355X; achieved HBM GB/s vs peak"
 GATV2_SLOPE = 0.2
+REDUCE_METRIC = "segment min/max aggregation GEdges/s at 1 MI355X; achieved HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2605_31500_amd", "csrc", "gt_attn.hip")
@@ -45,6 +48,74 @@ def gatv2_model_bytes(w) -> int:
     eb = 4 if w.dtype == "f32" else 2
     R = w.H * w.D * eb
     return 8 * (w.N + 1) + 4 * w.E + w.N * R + w.E * R + w.N * R + 4 * w.H * w.D
+
+
+def reduce_model_bytes(N: int, E: int, F: int, eb: int) -> int:
+    """Reduction: rowptr + colidx + one gathered feature row per CSR entry +
+    the output row and its int32 source indices per node."""
+    return 8 * (N + 1) + 4 * E + E * F * eb + N * F * eb + N * F * 4
+
+
+def run_reduce(args, w, gt, torch, to_device, synth) -> dict:
+    import numpy as np
+    F = args.features
+    X = synth.normal(1, synth.STREAM_Q, (w.N, F), 1.0, "f32")
+    rp, ci, x = (to_device(a) for a in (w.rowptr, w.colidx, X))
+    out = torch.empty_like(x)
+    arg = torch.empty(x.shape, dtype=torch.int32, device=x.device)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        gt.gt_segment_reduce(rp, ci, x, out, arg, op=args.reduce, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    gt.gt_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    phase_ms, calls = gt.gt_profile_collect()
+    gt.gt_profile_enable(False)
+    kern_ms = phase_ms[1] / calls
+    mbytes = reduce_model_bytes(w.N, w.E, F, 4)
+    achieved = mbytes / (kern_ms * 1e-3) / 1e9
+    rec = {
+        "metric": REDUCE_METRIC, "value": round(w.E / (ms * 1e-3) / 1e9, 4), "unit": "GEdges/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name.rsplit("-h", 1)[0] + "-f%d-f32" % F, "N": w.N, "E": w.E,
+                   "F": F, "op": args.reduce, "graph": w.name},
+        "roofline": {"bound": "hbm", "kernel": "gt_reduce_kernel", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": stored_traffic(w.name + ":reduce-%s-f%d" % (args.reduce, F)),
+                     "algorithmic_bytes_per_launch": mbytes, "kernel_ms": round(kern_ms, 5)},
+        "phases_ms": {"partition": round(phase_ms[0] / calls, 5), "reduce": round(kern_ms, 5),
+                      "merge": round(phase_ms[2] / calls, 5)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            oracle.segment_reduce(w.rowptr, w.colidx, X, args.reduce)
+            passes += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds:
+                break
+        rec["cpu_baseline"] = {"value": round(w.E * passes / el / 1e9, 6), "unit": "GEdges/s",
+                               "cores": oracle.threads(), "kind": "oracle",
+                               "sample": "all %d rows (%d CSR entries, %d features) of the same "
+                                         "workload, %d pass(es), %.1f s" % (w.N, w.E, F, passes, el)}
+    return rec
 
 
 def gatv2_attention_vector(w, seed: int):
@@ -177,6 +248,10 @@ def main() -> int:
                     help="time the backward pass (gt_attn_bwd) instead of the forward")
     ap.add_argument("--gatv2", action="store_true",
                     help="time the GATv2 forward (gt_gatv2_fwd) on the same graph")
+    ap.add_argument("--reduce", choices=["min", "max"], default=None,
+                    help="time the segment min/max aggregation (gt_segment_reduce)")
+    ap.add_argument("--features", type=int, default=512,
+                    help="features per node for --reduce (fp32; default 512)")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
                     help="enable the matrix-core path for dense 64-id windows holding at "
                          "least MIN in-window entries (bf16, H*D <= 128)")
@@ -203,6 +278,9 @@ def main() -> int:
     w = synth.config(args.config)
     if args.backward:
         print(json.dumps(run_backward(args, w, gt, torch, to_device, synth)), flush=True)
+        return 0
+    if args.reduce:
+        print(json.dumps(run_reduce(args, w, gt, torch, to_device, synth)), flush=True)
         return 0
     dev = [to_device(x) for x in (w.rowptr, w.colidx, w.Q, w.K, w.V)]
     out = torch.empty_like(dev[2])

@@ -192,6 +192,39 @@ gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* coli
                       int32_t H, int32_t D, float scale, hipStream_t stream);
 
 /*
+ * Segment min/max aggregation (paper Section 2.2, reduction family (ii):
+ * h_i <- REDUCE over the sources j of row i of h_j; Appendix, degree-aware
+ * reduction-based aggregation with the order-preserving (value, index) merge):
+ *
+ *     out[i,f] = the min (or max) over the CSR entries e of row i of X[j_e,f]
+ *     arg[i,f] = the source j_e that attains it
+ *
+ * Values are ordered by the paper's order-preserving key (the fp32 bit pattern
+ * with every bit inverted when the sign bit is set and the sign bit set
+ * otherwise, compared unsigned): non-NaN values in their real order, -0 below
+ * +0, a NaN with the sign bit clear above +inf and one with it set below -inf.
+ * Equal values resolve to the smallest source index, for min and for max.  An
+ * empty row gives out = 0 and arg = -1.  The result is exact (a selected input
+ * value) and does not depend on the row's entry order or on the tuning.
+ * Layouts: X, out [N][F] in `dtype` (16-byte aligned, no overlap); arg int32
+ * [N][F] (16-byte aligned) or NULL to skip it.  Supported F: rows of 64 B to
+ * 4 KiB in powers of two (fp32 F in {16, ..., 1024}, bf16 F in {32, ..., 2048}).
+ * tuning: light_max_deg, heavy_min_deg, chunk_edges and grid_blocks as for
+ * the attention forward (the degree-aware split of Appendix B.1 / D.1);
+ * dense_tiles is ignored.  Same ownership, workspace, asynchrony and error
+ * contract as gt_attn_fwd.
+ */
+typedef enum gt_reduce_op {
+    GT_REDUCE_MIN = 0,
+    GT_REDUCE_MAX = 1
+} gt_reduce_op;
+
+gt_status gt_segment_reduce(gt_dtype dtype, gt_reduce_op op, const int64_t* rowptr,
+                            const int32_t* colidx, const void* X, void* out, int32_t* arg,
+                            int64_t N, int64_t E, int32_t F, const gt_tuning* tuning,
+                            hipStream_t stream);
+
+/*
  * Debug utility, never on the attention path: checks on the device that
  * rowptr[0] == 0, rowptr is non-decreasing, rowptr[N] == E and every colidx
  * entry lies in [0, N).  Synchronous on `stream`; *valid (host memory) is set

@@ -25,8 +25,8 @@ GT_DTYPE_F32 = 0
 GT_DTYPE_BF16 = 1
 
 EXPORTED_SYMBOLS = (
-    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd", "gt_csr_validate",
-    "gt_status_string",
+    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
+    "gt_segment_reduce", "gt_csr_validate", "gt_status_string",
     "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
 )
 
@@ -63,6 +63,8 @@ def load_library(path: str = LIB_PATH):
     L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:6] + [P] + sig[6:-1] + [ctypes.POINTER(GtTuning), P]
     L.gt_gatv2_fwd.argtypes = [ctypes.c_int, P, P, P, P, P, f32, P, P, i64, i64, i32, i32,
                                ctypes.POINTER(GtTuning), P]
+    L.gt_segment_reduce.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, P, P, i64, i64, i32,
+                                    ctypes.POINTER(GtTuning), P]
     L.gt_attn_bwd.argtypes = [ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, P, i64, i64, i32, i32,
                               f32, P]
     L.gt_csr_validate.argtypes = [P, P, i64, i64, ctypes.POINTER(i32), P]
@@ -74,7 +76,7 @@ def load_library(path: str = LIB_PATH):
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     L.gt_workspace_release.argtypes = []
     for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
-                 "gt_csr_validate",
+                 "gt_segment_reduce", "gt_csr_validate",
                  "gt_profile_enable", "gt_profile_collect", "gt_workspace_release"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -180,6 +182,38 @@ def gt_gatv2_fwd(rowptr, colidx, L, R, att, slope, out, tuning=None, stream=None
     _check(load_library().gt_gatv2_fwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(L), _ptr(R),
                                        _ptr(att), float(slope), _ptr(out), _ptr(lse), N,
                                        colidx.numel(), H, D, tp, _stream(L.device, stream)))
+
+
+GT_REDUCE_OPS = {"min": 0, "max": 1}
+
+
+def gt_segment_reduce(rowptr, colidx, X, out, arg=None, op="min", tuning=None, stream=None) -> None:
+    """Segment min/max over each row's sources: out[i, f] and the source arg[i, f]
+    that attains it (see include/gt_attn.h).  X, out: [N, F] (dtype from X);
+    arg: int32 [N, F] device tensor or None."""
+    if X.dtype == torch.float32:
+        dtype, allowed = GT_DTYPE_F32, (torch.float32,)
+    else:
+        dtype, allowed = GT_DTYPE_BF16, (torch.bfloat16, torch.int16, torch.uint16)
+    for name, t in (("rowptr", rowptr), ("colidx", colidx), ("X", X), ("out", out)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(name + " must be a contiguous device tensor")
+    if rowptr.dtype != torch.int64 or colidx.dtype != torch.int32:
+        raise TypeError("rowptr must be int64 and colidx int32")
+    if X.dim() != 2 or out.shape != X.shape or X.dtype not in allowed or out.dtype != X.dtype:
+        raise ValueError("X and out must share one [N, F] shape and dtype")
+    N, F = X.shape
+    if rowptr.numel() != N + 1:
+        raise ValueError("rowptr must have N+1 entries")
+    if arg is not None and not (arg.is_cuda and arg.is_contiguous() and arg.dtype == torch.int32
+                                and tuple(arg.shape) == (N, F)):
+        raise ValueError("arg must be a contiguous int32 [N, F] device tensor")
+    if isinstance(tuning, dict):
+        tuning = GtTuning(**tuning)
+    tp = ctypes.byref(tuning) if tuning is not None else None
+    _check(load_library().gt_segment_reduce(dtype, GT_REDUCE_OPS[op], _ptr(rowptr), _ptr(colidx),
+                                            _ptr(X), _ptr(out), _ptr(arg), N, colidx.numel(), F,
+                                            tp, _stream(X.device, stream)))
 
 
 def gt_attn_bwd(rowptr, colidx, rowptr_t, colidx_t, Q, K, V, out, dout, lse, dQ, dK, dV, scale,

@@ -66,7 +66,7 @@ constexpr int kXcds = 8;
 // Score kinds of the attention skeleton.
 enum { KIND_GT = 0, KIND_GATV2 = 1 };
 
-enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_COUNT = 4 };
+enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_SLOTS = 4, CNT_COUNT = 5 };
 constexpr int kCntStride = 64;                          // ints between counters
 constexpr int kCntSetWords = CNT_COUNT * kCntStride;   // one counter set
 #define CNT(c, i) ((c)[(i) * kCntStride])
@@ -122,7 +122,7 @@ struct AttnParams {
     const float* att;  // GATv2 attention vector [H][D]
     float slope;       // GATv2 LeakyReLU negative slope
     int32_t light_max;
-    int32_t cap_chunks;
+    int32_t cap_items;
     const int32_t* counters;
     int32_t* next_counters;  // the other counter set, zeroed for the next call
     const int32_t* med_list;
@@ -139,7 +139,8 @@ struct PartParams {
     int32_t heavy_min;
     int32_t chunk;
     int32_t cap_heavy;
-    int32_t cap_chunks;
+    int32_t cap_items;  // work items: unsplit front rows + chunks of split rows
+    int32_t cap_slots;  // partial-state slots: chunks of split rows only
     int32_t* counters;
     int32_t* med_list;
     HeavyRow* heavy;
@@ -524,7 +525,7 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     // Counts come from the partition kernel; clamping keeps every list read
     // inside the workspace even if the CSR precondition were violated.
     if (blockIdx.x == 0 && threadIdx.x < CNT_COUNT) CNT(p.next_counters, threadIdx.x) = 0;
-    const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_chunks);
+    const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_items);
     const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
     const int nwaves = gridDim.x * kWavesPerBlock;
     for (int it = blockIdx.x * kWavesPerBlock + wv; it < n_items; it += nwaves) {
@@ -909,14 +910,14 @@ __device__ __forceinline__ int chunks_of(int64_t deg, int chunk) {
 
 __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     __shared__ int wave_cnt[kPartRowsPerThread][kWavesPerBlock];
-    __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock];
-    __shared__ int base[3];
+    __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock], scan_s[kWavesPerBlock];
+    __shared__ int base[4];
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const int64_t r0 = (int64_t)blockIdx.x * kPartRowsPerBlock;
     int64_t rb[kPartRowsPerThread], deg[kPartRowsPerThread];
     bool med[kPartRowsPerThread];
     uint64_t mask[kPartRowsPerThread];
-    int n_heavy = 0, n_chunk = 0;
+    int n_heavy = 0, n_chunk = 0, n_slot = 0;
 #pragma unroll
     for (int k = 0; k < kPartRowsPerThread; ++k) {
         const int64_t r = r0 + k * kBlock + threadIdx.x;
@@ -933,11 +934,13 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
             const int nch = chunks_of(deg[k], p.chunk);
             n_heavy += nch > 1 ? 1 : 0;
             n_chunk += nch;
+            n_slot += nch > 1 ? nch : 0;
         }
     }
-    int tot_h, tot_c;
+    int tot_h, tot_c, tot_s;
     const int off_h = block_exclusive_scan(n_heavy, scan_h, &tot_h);
     const int off_c = block_exclusive_scan(n_chunk, scan_c, &tot_c);
+    const int off_s = block_exclusive_scan(n_slot, scan_s, &tot_s);
     if (threadIdx.x == 0) {
         int tot_m = 0;
         for (int k = 0; k < kPartRowsPerThread; ++k)
@@ -945,10 +948,11 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
         base[0] = tot_m ? atomicAdd(&CNT(p.counters, CNT_MED), tot_m) : 0;
         base[1] = tot_h ? atomicAdd(&CNT(p.counters, CNT_HEAVY), tot_h) : 0;
         base[2] = tot_c ? atomicAdd(&CNT(p.counters, CNT_CHUNKS), tot_c) : 0;
+        base[3] = tot_s ? atomicAdd(&CNT(p.counters, CNT_SLOTS), tot_s) : 0;
     }
     __syncthreads();
     int pos = base[0];
-    int hid = base[1] + off_h, slot = base[2] + off_c;
+    int hid = base[1] + off_h, item = base[2] + off_c, slot = base[3] + off_s;
 #pragma unroll
     for (int k = 0; k < kPartRowsPerThread; ++k) {
         const int64_t r = r0 + k * kBlock + threadIdx.x;
@@ -959,26 +963,30 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
         if (deg[k] >= p.heavy_min) {
             // Rows of degree >= heavy_min are placed first in the work list (the
             // longest items start first).  A row that fits in one chunk is a
-            // single item writing its output directly; a longer row is split
-            // and recorded for the ordered merge.
+            // single item writing its output directly; a longer row is split,
+            // its chunks get partial-state slots, and it is recorded for the
+            // ordered merge.  Only split rows take slots, so the slots number
+            // at most 2E/chunk (a split row of degree d > chunk has fewer than
+            // 2d/chunk chunks).
             const int nch = chunks_of(deg[k], p.chunk);
-            const int need_h = nch > 1 ? 1 : 0;
-            if (hid + need_h > p.cap_heavy || slot + nch > p.cap_chunks) {
+            const int split = nch > 1 ? 1 : 0;
+            if (hid + split > p.cap_heavy || item + nch > p.cap_items || (split && slot + nch > p.cap_slots)) {
                 atomicOr(&CNT(p.counters, CNT_OVERFLOW), 1);
-            } else if (nch == 1) {
-                p.chunks[slot] = ChunkItem{(int32_t)r, -1, rb[k], rb[k] + deg[k]};
+            } else if (!split) {
+                p.chunks[item] = ChunkItem{(int32_t)r, -1, rb[k], rb[k] + deg[k]};
             } else {
                 const int64_t len = (deg[k] + nch - 1) / nch;
                 const int64_t end = rb[k] + deg[k];
                 p.heavy[hid] = HeavyRow{(int32_t)r, slot, nch, 0};
                 for (int c = 0; c < nch; ++c) {
                     const int64_t cb = rb[k] + c * len;
-                    p.chunks[slot + c] = ChunkItem{(int32_t)r, slot + c, cb < end ? cb : end,
+                    p.chunks[item + c] = ChunkItem{(int32_t)r, slot + c, cb < end ? cb : end,
                                                    cb + len < end ? cb + len : end};
                 }
             }
-            hid += need_h;
-            slot += nch;
+            hid += split;
+            item += nch;
+            slot += split ? nch : 0;
         }
     }
 }
@@ -1138,6 +1146,22 @@ struct Args {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Capacities of the partition's lists for E entries.  Split rows have degree
+// > chunk >= heavy_min, so they number at most E/heavy_min; front rows too.
+// A split row of degree d has fewer than 2d/chunk chunks, so work items are at
+// most E/heavy_min + 2E/chunk and partial-state slots at most 2E/chunk.
+struct PartCaps {
+    int64_t heavy, items, slots;
+};
+
+PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
+    PartCaps c;
+    c.heavy = E / heavy_min + 1;
+    c.slots = 2 * (E / chunk) + 1;
+    c.items = E / heavy_min + c.slots;
+    return c;
+}
+
 int device_cus(int dev) {
     static int cache[64] = {0};
     if (dev < 0 || dev >= 64) return 256;
@@ -1211,15 +1235,14 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     grid = (grid + kXcds - 1) / kXcds * kXcds;
 
     // workspace: counters | medium rows | heavy rows | chunk items | partial (m,l) | partial acc
-    const int64_t cap_heavy = a.E / heavy_min + 1;
-    const int64_t cap_chunks = a.E / chunk + cap_heavy + 1;
+    const PartCaps caps = part_caps(a.E, heavy_min, chunk);
     size_t off = 0;
     const size_t o_cnt = off;      off = align_up(off + 2 * kCntSetWords * sizeof(int32_t), 256);
     const size_t o_med = off;      off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
-    const size_t o_heavy = off;    off = align_up(off + (size_t)cap_heavy * sizeof(HeavyRow), 256);
-    const size_t o_chunks = off;   off = align_up(off + (size_t)cap_chunks * sizeof(ChunkItem), 256);
-    const size_t o_ml = off;       off = align_up(off + (size_t)cap_chunks * H * sizeof(float2), 256);
-    const size_t o_acc = off;      off = align_up(off + (size_t)cap_chunks * H * D * sizeof(float), 256);
+    const size_t o_heavy = off;    off = align_up(off + (size_t)caps.heavy * sizeof(HeavyRow), 256);
+    const size_t o_chunks = off;   off = align_up(off + (size_t)caps.items * sizeof(ChunkItem), 256);
+    const size_t o_ml = off;       off = align_up(off + (size_t)caps.slots * H * sizeof(float2), 256);
+    const size_t o_acc = off;      off = align_up(off + (size_t)caps.slots * H * D * sizeof(float), 256);
     const size_t ws_bytes = off;
 
     WsEntry& we = ws_entry(dev, stream);
@@ -1269,8 +1292,9 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.light_max = light_max;
     pp.heavy_min = heavy_min;
     pp.chunk = chunk;
-    pp.cap_heavy = (int32_t)cap_heavy;
-    pp.cap_chunks = (int32_t)cap_chunks;
+    pp.cap_heavy = (int32_t)caps.heavy;
+    pp.cap_items = (int32_t)caps.items;
+    pp.cap_slots = (int32_t)caps.slots;
     pp.counters = counters;
     pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
@@ -1312,7 +1336,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.att = a.att;
     ap.slope = a.slope;
     ap.light_max = light_max;
-    ap.cap_chunks = (int32_t)cap_chunks;
+    ap.cap_items = (int32_t)caps.items;
     ap.counters = counters;
     ap.next_counters = next_counters;
     ap.med_list = pp.med_list;
@@ -1325,14 +1349,14 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     if (prof) (void)hipEventRecord(ev[2], stream);
 
     MergeParams mp;
-    mp.cap_heavy = (int32_t)cap_heavy;
+    mp.cap_heavy = (int32_t)caps.heavy;
     mp.counters = counters;
     mp.heavy = pp.heavy;
     mp.part_acc = ap.part_acc;
     mp.part_ml = ap.part_ml;
     mp.out = ap.out;
     mp.lse = a.lse;
-    int merge_grid = (int)((cap_heavy + kWavesPerBlock - 1) / kWavesPerBlock);
+    int merge_grid = (int)((caps.heavy + kWavesPerBlock - 1) / kWavesPerBlock);
     const int merge_cap = device_cus(dev) * 8;
     if (merge_grid > merge_cap) merge_grid = merge_cap;
     if (merge_grid < 1) merge_grid = 1;
@@ -1447,6 +1471,37 @@ gt_status run_bwd(gt_dtype dtype, const BwdArgs& a, hipStream_t stream) {
     return fn(a, stream);
 }
 
+#include "gt_reduce.hpp"
+
+gt_status run_reduce(gt_dtype dtype, int op, const ReduceArgs& a0, const gt_tuning* tu, hipStream_t stream) {
+    t_last_error.clear();
+    if (dtype != GT_DTYPE_F32 && dtype != GT_DTYPE_BF16) return fail(GT_ERROR_NOT_SUPPORTED, "unknown dtype");
+    if (op != GT_REDUCE_MIN && op != GT_REDUCE_MAX) return fail(GT_ERROR_NOT_SUPPORTED, "unknown reduce op");
+    if (a0.N < 0 || a0.N >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "N must be in [0, 2^31)");
+    if (a0.E < 0 || a0.E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
+    if (a0.F < 1) return fail(GT_ERROR_INVALID_VALUE, "F must be positive");
+    ReduceFn fn = dtype == GT_DTYPE_F32 ? pick_reduce<float>(a0.F) : pick_reduce<bf16_tag>(a0.F);
+    if (!fn)
+        return fail(GT_ERROR_NOT_SUPPORTED, "unsupported F = " + std::to_string(a0.F) +
+                                                "; rows of 64 B to 4 KiB in powers of two (fp32 F in {16..1024}, "
+                                                "bf16 F in {32..2048})");
+    if (a0.N == 0) return GT_SUCCESS;
+    if (!a0.rowptr) return fail(GT_ERROR_INVALID_VALUE, "rowptr is null");
+    if (a0.E > 0 && !a0.colidx) return fail(GT_ERROR_INVALID_VALUE, "colidx is null");
+    if (!a0.X || !a0.out) return fail(GT_ERROR_INVALID_VALUE, "X and out must be non-null");
+    for (const void* ptr : {a0.X, static_cast<const void*>(a0.out), static_cast<const void*>(a0.arg)})
+        if (reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
+            return fail(GT_ERROR_INVALID_VALUE, "X, out and arg must be 16-byte aligned");
+    const size_t bytes = (size_t)a0.N * a0.F * (dtype == GT_DTYPE_F32 ? 4 : 2);
+    const size_t abytes = (size_t)a0.N * a0.F * sizeof(int32_t);
+    if (overlaps(a0.out, bytes, a0.X, bytes)) return fail(GT_ERROR_INVALID_VALUE, "out overlaps X");
+    if (a0.arg && (overlaps(a0.arg, abytes, a0.X, bytes) || overlaps(a0.arg, abytes, a0.out, bytes)))
+        return fail(GT_ERROR_INVALID_VALUE, "arg overlaps X or out");
+    ReduceArgs a = a0;
+    a.flip = op == GT_REDUCE_MAX ? 0xFFFFFFFFu : 0u;
+    return fn(a, tu, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1486,6 +1541,12 @@ gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* coli
     return run_bwd(dtype,
                    BwdArgs{rowptr, colidx, rowptr_t, colidx_t, Q, K, V, out, dout, lse, dQ, dK, dV, N, E, H, D, scale},
                    stream);
+}
+
+gt_status gt_segment_reduce(gt_dtype dtype, gt_reduce_op op, const int64_t* rowptr, const int32_t* colidx,
+                            const void* X, void* out, int32_t* arg, int64_t N, int64_t E, int32_t F,
+                            const gt_tuning* tuning, hipStream_t stream) {
+    return run_reduce(dtype, (int)op, ReduceArgs{rowptr, colidx, X, out, arg, N, E, F, 0u}, tuning, stream);
 }
 
 gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t N, int64_t E, int32_t* valid,

@@ -38,7 +38,7 @@ struct BwdParams {
     float c;      // scale * log2(e)
     float scale;
     int32_t light_max;
-    int32_t cap_chunks;
+    int32_t cap_items;
     int32_t cap_heavy;
     const int32_t* counters;
     int32_t* next_counters;
@@ -212,7 +212,7 @@ __global__ void __launch_bounds__(kBlock) gt_bwd_kernel(BwdParams p) {
     const int wv = threadIdx.x / kWave;
     int32_t* tile = tiles[wv];
     if (blockIdx.x == 0 && threadIdx.x < CNT_COUNT) CNT(p.next_counters, threadIdx.x) = 0;
-    const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_chunks);
+    const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_items);
     const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
     const int nwaves = gridDim.x * kWavesPerBlock;
     for (int it = blockIdx.x * kWavesPerBlock + wv; it < n_items; it += nwaves) {
@@ -344,14 +344,13 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
     if (g > need) g = need;
     const int grid = (int)(g > 0 ? g : 1);
 
-    const int64_t cap_heavy = a.E / heavy_min + 1;
-    const int64_t cap_chunks = a.E / chunk + cap_heavy + 1;
+    const PartCaps caps = part_caps(a.E, heavy_min, chunk);
     size_t off = 0;
     const size_t o_cnt = off;    off = align_up(off + 2 * kCntSetWords * sizeof(int32_t), 256);
     const size_t o_med = off;    off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
-    const size_t o_heavy = off;  off = align_up(off + (size_t)cap_heavy * sizeof(HeavyRow), 256);
-    const size_t o_chunks = off; off = align_up(off + (size_t)cap_chunks * sizeof(ChunkItem), 256);
-    const size_t o_part = off;   off = align_up(off + (size_t)cap_chunks * 2 * H * D * sizeof(float), 256);
+    const size_t o_heavy = off;  off = align_up(off + (size_t)caps.heavy * sizeof(HeavyRow), 256);
+    const size_t o_chunks = off; off = align_up(off + (size_t)caps.items * sizeof(ChunkItem), 256);
+    const size_t o_part = off;   off = align_up(off + (size_t)caps.slots * 2 * H * D * sizeof(float), 256);
     const size_t o_delta = off;  off = align_up(off + (size_t)a.N * H * sizeof(float), 256);
     const size_t ws_bytes = off;
 
@@ -391,8 +390,9 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
         pp.light_max = light_max;
         pp.heavy_min = heavy_min;
         pp.chunk = chunk;
-        pp.cap_heavy = (int32_t)cap_heavy;
-        pp.cap_chunks = (int32_t)cap_chunks;
+        pp.cap_heavy = (int32_t)caps.heavy;
+        pp.cap_items = (int32_t)caps.items;
+        pp.cap_slots = (int32_t)caps.slots;
         pp.counters = counters;
         pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
         pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
@@ -417,15 +417,15 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
         bp.c = a.scale * 1.4426950408889634f;
         bp.scale = a.scale;
         bp.light_max = light_max;
-        bp.cap_chunks = (int32_t)cap_chunks;
-        bp.cap_heavy = (int32_t)cap_heavy;
+        bp.cap_items = (int32_t)caps.items;
+        bp.cap_heavy = (int32_t)caps.heavy;
         bp.counters = counters;
         bp.next_counters = next_counters;
         bp.med_list = pp.med_list;
         bp.chunks = pp.chunks;
         bp.heavy = pp.heavy;
         bp.part = reinterpret_cast<float*>(ws + o_part);
-        int merge_grid = (int)((cap_heavy + kWavesPerBlock - 1) / kWavesPerBlock);
+        int merge_grid = (int)((caps.heavy + kWavesPerBlock - 1) / kWavesPerBlock);
         if (merge_grid > device_cus(dev) * 8) merge_grid = device_cus(dev) * 8;
         if (merge_grid < 1) merge_grid = 1;
         if (mode == 0) {

@@ -112,3 +112,29 @@ def test_gatv2_host_validation(lib, kw, status):
 
 def test_gatv2_empty_graph_is_a_no_op(lib):
     assert call_gatv2(lib, N=0, E=0) == 0
+
+
+def call_reduce(lib, dtype=0, op=0, rowptr=FAKE, colidx=FAKE, X=FAKE, out=FAKE + 0x100000,
+                arg=FAKE + 0x200000, N=10, E=20, F=64):
+    P = ctypes.c_void_p
+    return lib.gt_segment_reduce(dtype, op, P(rowptr), P(colidx), P(X), P(out), P(arg), N, E, F,
+                                 None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(F=48), 2), (dict(F=8), 2), (dict(F=2048), 2), (dict(dtype=1, F=16), 2),
+    (dict(dtype=1, F=4096), 2), (dict(op=2), 2), (dict(dtype=3), 2),
+    (dict(N=-1), 1), (dict(E=-1), 1), (dict(F=0), 1),
+    (dict(X=0), 1), (dict(out=0), 1), (dict(rowptr=0), 1), (dict(colidx=0), 1),
+    (dict(X=FAKE + 4), 1),                      # misaligned
+    (dict(arg=FAKE + 0x200008), 1),             # arg misaligned
+    (dict(out=FAKE + 1024), 1),                 # out overlaps X
+    (dict(arg=FAKE + 0x100000 + 256), 1),       # arg overlaps out
+])
+def test_reduce_host_validation(lib, kw, status):
+    assert call_reduce(lib, **kw) == status
+    assert lib.gt_last_error_message()
+
+
+def test_reduce_empty_graph_is_a_no_op(lib):
+    assert call_reduce(lib, N=0, E=0) == 0
