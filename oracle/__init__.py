@@ -58,6 +58,8 @@ def _load():
         L.gt_oracle_segment_reduce.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, i64, i64, i32,
                                                P, i64, P, P]
         L.gt_oracle_segment_reduce.restype = ctypes.c_int
+        L.gt_oracle_dot_aggr.argtypes = [P, P, P, i64, i64, i32, P, i64, P, P]
+        L.gt_oracle_dot_aggr.restype = ctypes.c_int
         L.gt_oracle_threads.argtypes = []
         L.gt_oracle_threads.restype = ctypes.c_int
         _lib = L
@@ -213,3 +215,26 @@ def segment_reduce(rowptr, colidx, X, op="min", rows=None):
     if rc:
         raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
     return out, arg
+
+
+def dot_aggr(rowptr, colidx, X, rows=None):
+    """Locality-study microbenchmark: s[i] = sum over row i's entries of <X[i], X[j]>.
+    X: [N, F] float32.  Returns (s, abs) float64 [nrows]; abs is the sum of the
+    absolute products (rounding-error scale)."""
+    rowptr = np.ascontiguousarray(rowptr, dtype=np.int64)
+    colidx = np.ascontiguousarray(colidx, dtype=np.int32)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    if X.ndim != 2:
+        raise ValueError("X must be [N, F]")
+    N, F = X.shape
+    if rowptr.size != N + 1:
+        raise ValueError("rowptr must have N+1 entries")
+    rows_arr = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    nrows = N if rows is None else rows_arr.size
+    out = np.empty(nrows)
+    absout = np.empty(nrows)
+    rc = _load().gt_oracle_dot_aggr(_ptr(rowptr), _ptr(colidx), _ptr(X), N, colidx.size, F,
+                                    _ptr(rows_arr), nrows, _ptr(out), _ptr(absout))
+    if rc:
+        raise ValueError("oracle: invalid arguments or CSR (code %d)" % rc)
+    return out, absout

@@ -493,3 +493,44 @@ int gt_oracle_segment_reduce(int dtype, int op, const int64_t* rowptr, const int
     }
     return status ? 2 : 0;
 }
+
+/*
+ * Locality microbenchmark of the reordering study (paper, graph reordering
+ * paragraph of Section 4 and its appendix figure: a "dot-aggr" kernel with
+ * identical arithmetic under two mappings).  Reading: for every row i,
+ *
+ *   s[i] = sum over the CSR entries e of row i of sum_f X[i,f] * X[j_e,f]
+ *
+ * (a repeated entry counts twice; an empty row gives 0), fp32 X.  absout[i]
+ * = the same sum of |X[i,f] * X[j_e,f]|, the scale of any floating-point
+ * evaluation's rounding error.
+ */
+int gt_oracle_dot_aggr(const int64_t* rowptr, const int32_t* colidx, const float* X, int64_t N,
+                       int64_t E, int32_t F, const int64_t* rows, int64_t nrows, double* out,
+                       double* absout) {
+    if (N < 0 || E < 0 || F < 1 || nrows < 0 || !rowptr || (nrows > 0 && !out) ||
+        (E > 0 && !colidx) || (N > 0 && !X) || (!rows && nrows != N))
+        return 1;
+    if (rowptr[0] != 0 || rowptr[N] != E) return 2;
+    int status = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : status)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows ? rows[r] : r;
+        if (i < 0 || i >= N) { status |= 2; continue; }
+        const int64_t b = rowptr[i], e = rowptr[i + 1];
+        if (b < 0 || e < b || e > E) { status |= 2; continue; }
+        double s = 0.0, a = 0.0;
+        for (int64_t t = b; t < e; ++t) {
+            const int64_t j = colidx[t];
+            if (j < 0 || j >= N) { status |= 2; break; }
+            for (int32_t f = 0; f < F; ++f) {
+                const double p = (double)X[i * F + f] * (double)X[j * F + f];
+                s += p;
+                a += fabs(p);
+            }
+        }
+        out[r] = s;
+        if (absout) absout[r] = a;
+    }
+    return status ? 2 : 0;
+}

@@ -324,3 +324,43 @@ def transpose_csr(rowptr: np.ndarray, colidx: np.ndarray, N: int):
     rowptr_t = np.zeros(N + 1, dtype=np.int64)
     np.cumsum(np.bincount(colidx, minlength=N), out=rowptr_t[1:])
     return rowptr_t, colidx_t
+
+
+# ------------------------------------------------------------ node orderings
+# Relabelings for the locality study: new node k is old node perm[k].
+
+def permute_graph(rowptr: np.ndarray, colidx: np.ndarray, perm: np.ndarray):
+    """CSR of the relabeled graph: row k is old row perm[k] with every source
+    mapped to its new id; each row keeps its entry order.  Features follow
+    with X[perm]."""
+    N = rowptr.size - 1
+    perm = np.ascontiguousarray(perm, dtype=np.int64)
+    if perm.size != N or not np.array_equal(np.sort(perm), np.arange(N)):
+        raise ValueError("perm must be a permutation of 0..N-1")
+    inv = np.empty(N, dtype=np.int64)
+    inv[perm] = np.arange(N)
+    deg = np.diff(rowptr)[perm]
+    new_rowptr = np.zeros(N + 1, dtype=np.int64)
+    np.cumsum(deg, out=new_rowptr[1:])
+    # gather the old rows in the new order, then map their sources
+    starts = rowptr[:-1][perm]
+    idx = np.repeat(starts - new_rowptr[:-1], deg) + np.arange(new_rowptr[-1])
+    new_colidx = inv[colidx[idx]].astype(np.int32)
+    return new_rowptr, new_colidx
+
+
+def random_order(seed: int, N: int) -> np.ndarray:
+    """A uniformly random relabeling (argsort of seeded uniforms)."""
+    return np.argsort(uniform01(seed, STREAM_PERM, N), kind="stable")
+
+
+def rcm_order(rowptr: np.ndarray, colidx: np.ndarray) -> np.ndarray:
+    """Reverse Cuthill-McKee order of the symmetrized graph (scipy): a
+    bandwidth-reducing relabeling that places neighbourhoods at nearby ids,
+    standing in for partition-based reorderings such as METIS."""
+    import scipy.sparse as sp
+    from scipy.sparse.csgraph import reverse_cuthill_mckee
+    N = rowptr.size - 1
+    A = sp.csr_matrix((np.ones(colidx.size, dtype=np.int8), colidx, rowptr), shape=(N, N))
+    S = (A + A.T).tocsr()
+    return np.asarray(reverse_cuthill_mckee(S, symmetric_mode=True), dtype=np.int64)
