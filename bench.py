@@ -14,7 +14,11 @@ times the GATv2 forward (same skeleton, score a^T LeakyReLU(l_i + r_j), one
 gathered row per entry) on the same graph, with L, R the workload's first two
 feature tensors and a N(0, 1/D) attention vector; ``--reduce min|max`` times
 the segment min/max aggregation with its selected sources over the same graph
-with ``--features`` (default 512) fp32 N(0,1) features per node.
+with ``--features`` (default 512) fp32 N(0,1) features per node;
+``--study-reorder`` runs the locality study instead (the dot-aggr
+microbenchmark under both mappings and load widths on original, random and
+reverse Cuthill-McKee node orders, plus the attention forward under each
+order) and prints one JSON line per measurement.
 """
 from __future__ import annotations
 
@@ -116,6 +120,73 @@ def run_reduce(args, w, gt, torch, to_device, synth) -> dict:
                                "sample": "all %d rows (%d CSR entries, %d features) of the same "
                                          "workload, %d pass(es), %.1f s" % (w.N, w.E, F, passes, el)}
     return rec
+
+
+def _time_calls(torch, fn, steps: int) -> float:
+    """Average ms per call over `steps` calls after one warm-up call."""
+    fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def run_study(args, gt, torch, to_device, synth) -> int:
+    """Reordering gap (paper, graph-reordering study): s = t_original /
+    t_reordered per kernel variant, gap = s_neighbour - s_feature."""
+    import numpy as np
+    configs = [int(c) for c in args.study_configs.split(",")]
+    fs = [int(f) for f in args.study_features.split(",")]
+    variants = [("feature", 4), ("feature", 16), ("neighbor", 4), ("neighbor", 16)]
+    for c in configs:
+        w = synth.config(c)
+        t0 = time.perf_counter()
+        orders = {"original": None, "random": synth.random_order(7, w.N),
+                  "rcm": synth.rcm_order(w.rowptr, w.colidx)}
+        graphs = {k: (w.rowptr, w.colidx) if p is None else synth.permute_graph(w.rowptr, w.colidx, p)
+                  for k, p in orders.items()}
+        print(json.dumps({"study": "orders", "graph": w.name, "N": w.N, "E": w.E,
+                          "seconds": round(time.perf_counter() - t0, 1)}), flush=True)
+        # attention forward under each order (the workload's own features, permuted)
+        times = {}
+        for k, p in orders.items():
+            rp, ci = graphs[k]
+            feats = [w.Q, w.K, w.V] if p is None else [np.ascontiguousarray(a[p]) for a in (w.Q, w.K, w.V)]
+            dev = [to_device(a) for a in [rp, ci] + feats]
+            out = torch.empty_like(dev[2])
+            times[k] = _time_calls(torch, lambda: gt.gt_attn_fwd_ex(*dev, out, w.scale), args.steps)
+            del dev, out
+        print(json.dumps({"study": "attention", "graph": w.name,
+                          "ms": {k: round(v, 4) for k, v in times.items()},
+                          "s_rcm": round(times["original"] / times["rcm"], 3),
+                          "s_random": round(times["original"] / times["random"], 3)}), flush=True)
+        for F in fs:
+            X = synth.normal(1, synth.STREAM_Q, (w.N, F), 1.0, "f32")
+            res = {}
+            for k, p in orders.items():
+                rp, ci = (to_device(a) for a in graphs[k])
+                x = to_device(X if p is None else np.ascontiguousarray(X[p]))
+                out = torch.empty(w.N, dtype=torch.float32, device=x.device)
+                for m, vb in variants:
+                    res[(m, vb, k)] = _time_calls(
+                        torch, lambda: gt.gt_dot_aggr(rp, ci, x, out, mapping=m, load_bytes=vb), args.steps)
+                del rp, ci, x, out
+                torch.cuda.empty_cache()
+            for vb in (4, 16):
+                rec = {"study": "dot-aggr", "graph": w.name, "F": F, "load_bytes": vb}
+                for m in ("feature", "neighbor"):
+                    rec[m + "_ms"] = {k: round(res[(m, vb, k)], 4) for k in orders}
+                    rec["s_" + m] = {k: round(res[(m, vb, "original")] / res[(m, vb, k)], 3)
+                                     for k in ("rcm", "random")}
+                rec["gap"] = {k: round(rec["s_neighbor"][k] - rec["s_feature"][k], 3)
+                              for k in ("rcm", "random")}
+                print(json.dumps(rec), flush=True)
+    return 0
 
 
 def gatv2_attention_vector(w, seed: int):
@@ -229,10 +300,16 @@ def copy_calibration(mib: int, steps: int) -> int:
     src = torch.ones(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
     for _ in range(steps):
         dst.copy_(src)
+    e1.record()
     torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": steps}))
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": steps,
+                      "ms_per_copy": round(ms, 4), "copy_GBps": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}))
     return 0
 
 
@@ -252,6 +329,10 @@ def main() -> int:
                     help="time the segment min/max aggregation (gt_segment_reduce)")
     ap.add_argument("--features", type=int, default=512,
                     help="features per node for --reduce (fp32; default 512)")
+    ap.add_argument("--study-reorder", action="store_true",
+                    help="run the locality study (dot-aggr mappings x load widths x node orders)")
+    ap.add_argument("--study-configs", default="1,2,3,4", help="graphs of the study (indices)")
+    ap.add_argument("--study-features", default="32,128,512", help="feature widths of the study")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
                     help="enable the matrix-core path for dense 64-id windows holding at "
                          "least MIN in-window entries (bf16, H*D <= 128)")
@@ -275,6 +356,8 @@ def main() -> int:
     import paper_2605_31500_amd as gt
     from tests.helpers import to_device
 
+    if args.study_reorder:
+        return run_study(args, gt, torch, to_device, synth)
     w = synth.config(args.config)
     if args.backward:
         print(json.dumps(run_backward(args, w, gt, torch, to_device, synth)), flush=True)

@@ -225,6 +225,28 @@ gt_status gt_segment_reduce(gt_dtype dtype, gt_reduce_op op, const int64_t* rowp
                             hipStream_t stream);
 
 /*
+ * Locality microbenchmark of the paper's reordering study (Section 4, graph
+ * reordering; the appendix figure of the reordering gap): the "dot-aggr"
+ * kernel, read here as
+ *
+ *     out[i] = sum over the CSR entries e of row i of sum_f X[i,f] * X[j_e,f]
+ *
+ * (fp32; an empty row gives 0), evaluated by one wavefront per row under one
+ * of two mappings with identical arithmetic:
+ *   mapping 0, feature-parallel: lanes span the features, neighbours are
+ *              scanned in turn (coalesced loads of one neighbour row);
+ *   mapping 1, neighbour-parallel: each lane takes its own neighbours and
+ *              reads their whole rows (gather-like loads).
+ * load_bytes selects scalar (4) or vectorised (16) loads per lane.  F in {32,
+ * 64, 128, 256, 512}.  X [N][F] fp32, 16-byte aligned; out float [N].  The
+ * sum order differs between variants (fp32 accumulation per lane, then a tree
+ * over the wavefront).  Asynchronous on `stream`; no workspace.
+ */
+gt_status gt_dot_aggr(const int64_t* rowptr, const int32_t* colidx, const float* X, float* out,
+                      int64_t N, int64_t E, int32_t F, int32_t mapping, int32_t load_bytes,
+                      hipStream_t stream);
+
+/*
  * Debug utility, never on the attention path: checks on the device that
  * rowptr[0] == 0, rowptr is non-decreasing, rowptr[N] == E and every colidx
  * entry lies in [0, N).  Synchronous on `stream`; *valid (host memory) is set

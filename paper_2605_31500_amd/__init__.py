@@ -26,7 +26,7 @@ GT_DTYPE_BF16 = 1
 
 EXPORTED_SYMBOLS = (
     "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
-    "gt_segment_reduce", "gt_csr_validate", "gt_status_string",
+    "gt_segment_reduce", "gt_dot_aggr", "gt_csr_validate", "gt_status_string",
     "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
 )
 
@@ -65,6 +65,7 @@ def load_library(path: str = LIB_PATH):
                                ctypes.POINTER(GtTuning), P]
     L.gt_segment_reduce.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, P, P, i64, i64, i32,
                                     ctypes.POINTER(GtTuning), P]
+    L.gt_dot_aggr.argtypes = [P, P, P, P, i64, i64, i32, i32, i32, P]
     L.gt_attn_bwd.argtypes = [ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P, P, P, i64, i64, i32, i32,
                               f32, P]
     L.gt_csr_validate.argtypes = [P, P, i64, i64, ctypes.POINTER(i32), P]
@@ -76,7 +77,7 @@ def load_library(path: str = LIB_PATH):
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     L.gt_workspace_release.argtypes = []
     for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
-                 "gt_segment_reduce", "gt_csr_validate",
+                 "gt_segment_reduce", "gt_dot_aggr", "gt_csr_validate",
                  "gt_profile_enable", "gt_profile_collect", "gt_workspace_release"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -182,6 +183,25 @@ def gt_gatv2_fwd(rowptr, colidx, L, R, att, slope, out, tuning=None, stream=None
     _check(load_library().gt_gatv2_fwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(L), _ptr(R),
                                        _ptr(att), float(slope), _ptr(out), _ptr(lse), N,
                                        colidx.numel(), H, D, tp, _stream(L.device, stream)))
+
+
+DOT_MAPPINGS = {"feature": 0, "neighbor": 1}
+
+
+def gt_dot_aggr(rowptr, colidx, X, out, mapping="feature", load_bytes=16, stream=None) -> None:
+    """Locality-study microbenchmark: out[i] = sum over row i's entries of <X[i], X[j]>.
+    X: float32 [N, F] device tensor; out: float32 [N]."""
+    for name, t in (("rowptr", rowptr), ("colidx", colidx), ("X", X), ("out", out)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(name + " must be a contiguous device tensor")
+    if X.dtype != torch.float32 or out.dtype != torch.float32 or X.dim() != 2:
+        raise TypeError("X must be float32 [N, F] and out float32 [N]")
+    N, F = X.shape
+    if out.numel() != N or rowptr.numel() != N + 1:
+        raise ValueError("out must have N entries and rowptr N+1")
+    _check(load_library().gt_dot_aggr(_ptr(rowptr), _ptr(colidx), _ptr(X), _ptr(out), N,
+                                      colidx.numel(), F, DOT_MAPPINGS[mapping], int(load_bytes),
+                                      _stream(X.device, stream)))
 
 
 GT_REDUCE_OPS = {"min": 0, "max": 1}

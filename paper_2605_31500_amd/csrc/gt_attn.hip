@@ -1502,6 +1502,31 @@ gt_status run_reduce(gt_dtype dtype, int op, const ReduceArgs& a0, const gt_tuni
     return fn(a, tu, stream);
 }
 
+#include "gt_study.hpp"
+
+gt_status run_dot_aggr(const int64_t* rowptr, const int32_t* colidx, const float* X, float* out, int64_t N,
+                       int64_t E, int32_t F, int32_t mapping, int32_t load_bytes, hipStream_t stream) {
+    t_last_error.clear();
+    if (N < 0 || N >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "N must be in [0, 2^31)");
+    if (E < 0 || E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
+    DotFn fn = pick_dot(mapping, load_bytes, F);
+    if (!fn)
+        return fail(GT_ERROR_NOT_SUPPORTED, "unsupported dot-aggr variant: mapping in {0, 1}, load_bytes in "
+                                            "{4, 16}, F in {32, 64, 128, 256, 512}");
+    if (N == 0) return GT_SUCCESS;
+    if (!rowptr || (E > 0 && !colidx) || !X || !out) return fail(GT_ERROR_INVALID_VALUE, "null pointer");
+    if (reinterpret_cast<uintptr_t>(X) % 16 != 0 || reinterpret_cast<uintptr_t>(out) % 4 != 0)
+        return fail(GT_ERROR_INVALID_VALUE, "X must be 16-byte and out 4-byte aligned");
+    if (overlaps(out, (size_t)N * sizeof(float), X, (size_t)N * F * sizeof(float)))
+        return fail(GT_ERROR_INVALID_VALUE, "out overlaps X");
+    DotParams dp{rowptr, colidx, X, out, N};
+    const int64_t blocks = (N + kWavesPerBlock - 1) / kWavesPerBlock;
+    hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, dp);
+    const hipError_t he = hipGetLastError();
+    if (he != hipSuccess) return hip_fail(he, "dot-aggr launch");
+    return GT_SUCCESS;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1547,6 +1572,11 @@ gt_status gt_segment_reduce(gt_dtype dtype, gt_reduce_op op, const int64_t* rowp
                             const void* X, void* out, int32_t* arg, int64_t N, int64_t E, int32_t F,
                             const gt_tuning* tuning, hipStream_t stream) {
     return run_reduce(dtype, (int)op, ReduceArgs{rowptr, colidx, X, out, arg, N, E, F, 0u}, tuning, stream);
+}
+
+gt_status gt_dot_aggr(const int64_t* rowptr, const int32_t* colidx, const float* X, float* out, int64_t N,
+                      int64_t E, int32_t F, int32_t mapping, int32_t load_bytes, hipStream_t stream) {
+    return run_dot_aggr(rowptr, colidx, X, out, N, E, F, mapping, load_bytes, stream);
 }
 
 gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t N, int64_t E, int32_t* valid,

@@ -138,3 +138,18 @@ def test_reduce_host_validation(lib, kw, status):
 
 def test_reduce_empty_graph_is_a_no_op(lib):
     assert call_reduce(lib, N=0, E=0) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(F=48), 2), (dict(F=1024), 2), (dict(mapping=2), 2), (dict(load_bytes=8), 2),
+    (dict(N=-1), 1), (dict(X=0), 1), (dict(out=0), 1), (dict(X=FAKE + 4), 1),
+    (dict(out=FAKE + 2), 1), (dict(out=FAKE + 64), 1),   # misaligned out; out overlaps X
+])
+def test_dot_aggr_host_validation(lib, kw, status):
+    a = dict(rowptr=FAKE, colidx=FAKE, X=FAKE, out=FAKE + 0x200000, N=10, E=20, F=64, mapping=0,
+             load_bytes=16)
+    a.update(kw)
+    P = ctypes.c_void_p
+    assert lib.gt_dot_aggr(P(a["rowptr"]), P(a["colidx"]), P(a["X"]), P(a["out"]), a["N"], a["E"],
+                           a["F"], a["mapping"], a["load_bytes"], None) == status
+    assert lib.gt_last_error_message()
