@@ -36,7 +36,7 @@ GATV2_SLOPE = 0.2
 REDUCE_METRIC = "segment min/max aggregation GEdges/s at 1 MI355X; achieved HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2605_31500_amd", "csrc", "gt_attn.hip")
+KERNEL_SRC_DIR = os.path.join(ROOT, "paper_2605_31500_amd", "csrc")
 
 
 def model_bytes(w) -> int:
@@ -257,7 +257,14 @@ def run_backward(args, w, gt, torch, to_device, synth) -> dict:
 
 
 def source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    """Hash of the library's HIP sources (the .hip file and the headers it
+    includes, in name order): counter readings are tied to this."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_SRC_DIR)):
+        if name.endswith((".hip", ".hpp")):
+            h.update(name.encode())
+            h.update(open(os.path.join(KERNEL_SRC_DIR, name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def stored_traffic(workload: str):

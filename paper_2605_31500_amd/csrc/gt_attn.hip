@@ -872,15 +872,13 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
     }
 }
 
-// Degree binning.  A block owns kPartRowsPerBlock contiguous rows; thread t
-// takes rows t, t+256, ... of the block, so every rowptr load is coalesced.
-// Medium rows are compacted with wave ballots; heavy-row and chunk counts
-// with block scans; each block then reserves its output ranges with one
-// atomic per list.  A heavy row is cut into at most kMaxChunks chunks of
-// (about) equal length, at least `chunk` entries each, so the ordered merge
-// of a hub stays a few load rounds long.
-constexpr int kPartRowsPerThread = 8;
-constexpr int kPartRowsPerBlock = kBlock * kPartRowsPerThread;
+// Degree binning.  A block owns RPT * 256 contiguous rows; thread t takes
+// rows t, t+256, ... of the block, so every rowptr load is coalesced.  Medium
+// rows are compacted with wave ballots; heavy-row and chunk counts with block
+// scans; each block then reserves its output ranges with one atomic per list.
+// A heavy row is cut into at most kMaxChunks chunks of (about) equal length,
+// at least `chunk` entries each, so the ordered merge of a hub stays a few
+// load rounds long.
 constexpr int kMaxChunks = 32;
 
 __device__ __forceinline__ int block_exclusive_scan(int v, int* lds_waves, int* total) {
@@ -908,7 +906,10 @@ __device__ __forceinline__ int chunks_of(int64_t deg, int chunk) {
     return (int)(n < kMaxChunks ? n : kMaxChunks);
 }
 
+template <int RPT>
 __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
+    constexpr int kPartRowsPerThread = RPT;
+    constexpr int kPartRowsPerBlock = kBlock * RPT;
     __shared__ int wave_cnt[kPartRowsPerThread][kWavesPerBlock];
     __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock], scan_s[kWavesPerBlock];
     __shared__ int base[4];
@@ -989,6 +990,22 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
             slot += split ? nch : 0;
         }
     }
+}
+
+// Launches the degree binning over pp.N rows.  The blocks' list reservations
+// (one atomic per list and block) serialise on the list counters, so large
+// graphs take 2048 rows per block; smaller ones take 1024, giving more blocks
+// in parallel.  Measured on MI355X: 169K rows 12.8 -> 10.5 us with 1024;
+// 2.1M rows 32 -> 44 us with 1024.
+hipError_t launch_partition(const PartParams& pp, hipStream_t stream) {
+    if (pp.N <= (int64_t(1) << 19)) {
+        const int grid = (int)((pp.N + 4 * kBlock - 1) / (4 * kBlock));
+        hipLaunchKernelGGL(gt_partition_kernel<4>, dim3(grid), dim3(kBlock), 0, stream, pp);
+    } else {
+        const int grid = (int)((pp.N + 8 * kBlock - 1) / (8 * kBlock));
+        hipLaunchKernelGGL(gt_partition_kernel<8>, dim3(grid), dim3(kBlock), 0, stream, pp);
+    }
+    return hipGetLastError();
 }
 
 // Merge of the chunk partials of each heavy row, in chunk order (one
@@ -1299,9 +1316,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
-    const int part_grid = (int)((a.N + kPartRowsPerBlock - 1) / kPartRowsPerBlock);
-    hipLaunchKernelGGL(gt_partition_kernel, dim3(part_grid), dim3(kBlock), 0, stream, pp);
-    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "partition launch");
+    if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
     if constexpr (kTileShape) {
         if (tiles) {
             TileParams tp;

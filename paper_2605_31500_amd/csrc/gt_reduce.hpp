@@ -461,9 +461,7 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
-    const int part_grid = (int)((a.N + kPartRowsPerBlock - 1) / kPartRowsPerBlock);
-    hipLaunchKernelGGL(gt_partition_kernel, dim3(part_grid), dim3(kBlock), 0, stream, pp);
-    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "partition launch");
+    if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
     if (prof) (void)hipEventRecord(ev[1], stream);
 
     ReduceParams rp;
