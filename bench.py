@@ -18,7 +18,9 @@ with ``--features`` (default 512) fp32 N(0,1) features per node;
 ``--study-reorder`` runs the locality study instead (the dot-aggr
 microbenchmark under both mappings and load widths on original, random and
 reverse Cuthill-McKee node orders, plus the attention forward under each
-order) and prints one JSON line per measurement.
+order) and prints one JSON line per measurement; ``--ablate-degree`` times the
+attention forward under the degree-aware partition and two degree-agnostic
+mappings (one lane group per row; one wavefront per row).
 """
 from __future__ import annotations
 
@@ -189,6 +191,43 @@ def run_study(args, gt, torch, to_device, synth) -> int:
     return 0
 
 
+ABLATION_MODES = {
+    # the default degree-aware partition
+    "degree_aware": None,
+    # degree-agnostic: every row on one lane group, no split (one sub-wavefront per node)
+    "group_per_row": {"light_max_deg": 1 << 30, "heavy_min_deg": (1 << 30) + 1},
+    # degree-agnostic: every row of degree >= 2 on one wavefront, no split
+    # (the tuning interface keeps rows of degree <= 1 on lane groups)
+    "wave_per_row": {"light_max_deg": 1, "heavy_min_deg": 1 << 30},
+}
+
+
+def run_ablation(args, gt, torch, to_device, synth) -> int:
+    """Degree-aware versus degree-agnostic work allocation (the paper's
+    ablation of its degree-aware warp allocation): the same attention kernel
+    under the default partition and under two degree-agnostic mappings,
+    speed-up = t_agnostic / t_aware, one JSON line per graph."""
+    for c in [int(x) for x in args.ablate_configs.split(",")]:
+        w = synth.config(c)
+        dev = [to_device(a) for a in (w.rowptr, w.colidx, w.Q, w.K, w.V)]
+        out = torch.empty_like(dev[2])
+        ms = {}
+        for _ in range(3):  # interleaved rounds; the fastest round of each mode counts
+            for mode, tu in ABLATION_MODES.items():
+                t = _time_calls(torch, lambda: gt.gt_attn_fwd_ex(*dev, out, w.scale, tuning=tu),
+                                args.steps)
+                ms[mode] = min(ms.get(mode, t), t)
+        print(json.dumps({"ablation": "degree-aware allocation", "graph": w.name, "N": w.N, "E": w.E,
+                          "max_degree": int((w.rowptr[1:] - w.rowptr[:-1]).max()),
+                          "ms_per_call": {k: round(v, 4) for k, v in ms.items()},
+                          "speedup_vs_group_per_row": round(ms["group_per_row"] / ms["degree_aware"], 3),
+                          "speedup_vs_wave_per_row": round(ms["wave_per_row"] / ms["degree_aware"], 3)}),
+              flush=True)
+        del dev, out
+        torch.cuda.empty_cache()
+    return 0
+
+
 def gatv2_attention_vector(w, seed: int):
     import math
     import synth
@@ -339,6 +378,9 @@ def main() -> int:
     ap.add_argument("--study-reorder", action="store_true",
                     help="run the locality study (dot-aggr mappings x load widths x node orders)")
     ap.add_argument("--study-configs", default="1,2,3,4", help="graphs of the study (indices)")
+    ap.add_argument("--ablate-degree", action="store_true",
+                    help="time degree-aware versus degree-agnostic work allocation")
+    ap.add_argument("--ablate-configs", default="1,2,3,4", help="graphs of the ablation (indices)")
     ap.add_argument("--study-features", default="32,128,512", help="feature widths of the study")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
                     help="enable the matrix-core path for dense 64-id windows holding at "
@@ -365,6 +407,8 @@ def main() -> int:
 
     if args.study_reorder:
         return run_study(args, gt, torch, to_device, synth)
+    if args.ablate_degree:
+        return run_ablation(args, gt, torch, to_device, synth)
     w = synth.config(args.config)
     if args.backward:
         print(json.dumps(run_backward(args, w, gt, torch, to_device, synth)), flush=True)

@@ -85,7 +85,11 @@ gt_status gt_attn_fwd(const int64_t* rowptr, const int32_t* colidx, const float*
 
 /*
  * bf16 features given as uint16 bit patterns; fp32 accumulation; bf16 output
- * rounded to nearest even.  Otherwise identical to gt_attn_fwd.
+ * rounded to nearest even.  Scores are bf16 dot products accumulated in fp32;
+ * each softmax weight is rounded to bf16 before it multiplies its value row,
+ * while the normaliser (and lse) sums the fp32 weights; the largest weight of
+ * a row is exactly 1, so a single-entry row returns its value exactly.
+ * Otherwise identical to gt_attn_fwd.
  */
 gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const uint16_t* Q,
                            const uint16_t* K, const uint16_t* V, uint16_t* out, int64_t N,

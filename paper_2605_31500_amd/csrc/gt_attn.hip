@@ -220,6 +220,28 @@ template <int HL> __device__ __forceinline__ float head_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// bf16 pair arithmetic (gfx950 v_dot2c_f32_bf16, v_cvt_pk_bf16_f32, v_perm_b32).
+// A dword holds bf16 element 2k in its low half and 2k+1 in its high half.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// c + a.lo * b.lo + a.hi * b.hi, products of bf16 pairs accumulated in fp32
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c,
+                                           false);
+}
+
+// two fp32 values rounded to nearest even bf16, x in the low half
+__device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
+    bf16x2_t r;
+    r[0] = (__bf16)x;
+    r[1] = (__bf16)y;
+    return __builtin_bit_cast(uint32_t, r);
+}
+
+// (a.lo, b.lo) and (a.hi, b.hi): the same element of two rows as one pair
+__device__ __forceinline__ uint32_t pair_lo(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x05040100u); }
+__device__ __forceinline__ uint32_t pair_hi(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+
 // Orders LDS traffic of one wavefront around a tile hand-off (the hardware
 // executes a wave's LDS operations in order; this stops compiler reordering).
 __device__ __forceinline__ void wave_lds_fence() {
@@ -246,12 +268,22 @@ template <typename T, int H, int D, int KIND = KIND_GT>
 struct RowState {
     using Gm = Geo<T, H, D>;
     static constexpr bool kGat = KIND == KIND_GATV2;
+    // bf16 graph-transformer rows: scores with bf16 dot2 on the raw Q and K
+    // pairs, and P*V with the weights of two entries rounded to one bf16 pair
+    // and dot2 against the two entries' values: about half the vector
+    // instructions of widening every element to fp32.  The normaliser sums
+    // the fp32 weights, so lse keeps fp32 accuracy; the rounded weights then
+    // sum to within 2^-9 of it, which bounds the extra error of out by
+    // 2^-9 * sum_e p_e |v_e| / sum_e p_e.
+    static constexpr bool kDot2 = std::is_same<T, bf16_tag>::value && !kGat;
+    static_assert(!kDot2 || Gm::kU % 2 == 0, "dot2 pairs entries");
     float q[Gm::kNV][Gm::kEPV];
     float a[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
     float a2[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
     float acc[Gm::kNV][Gm::kEPV];
     float m[Gm::kNV];  // running max of log2-scaled scores for this lane's head
     float l[Gm::kNV];  // running sum of 2^(s - m)
+    uint4 qraw[kDot2 ? Gm::kNV : 1];  // the row vector as bf16 pairs (dot2 form)
 
     __device__ __forceinline__ void begin(const char* __restrict__ Qb, int64_t row, int lig,
                                           const float* __restrict__ att = nullptr, float slope = 0.0f) {
@@ -259,7 +291,10 @@ struct RowState {
 #pragma unroll
         for (int k = 0; k < Gm::kNV; ++k) {
             const uint4 r = *reinterpret_cast<const uint4*>(qrow + k * Gm::kG * 16);
-            widen<T>(r, q[k]);
+            if constexpr (kDot2)
+                qraw[k] = r;
+            else
+                widen<T>(r, q[k]);
             if constexpr (kGat) {
                 // the attention vector is [H][D] fp32 in the row's element order
                 const float* av = att + (lig + k * Gm::kG) * Gm::kEPV;
@@ -309,6 +344,10 @@ struct RowState {
         // subtraction of the running max would give the maximal entry a weight
         // of 2^(rounding error) instead of exactly 1.
 #pragma clang fp contract(off)
+        if constexpr (kDot2) {
+            consume_dot2(bt, nvalid, c);
+            return;
+        }
         constexpr int U = Gm::kU;
         float s[U][Gm::kNV];
 #pragma unroll
@@ -353,6 +392,54 @@ struct RowState {
                     widen<T>(bt.v[u][k], vf);
 #pragma unroll
                 for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = fmaf(pu, vf[e], acc[k][e]);
+            }
+            m[k] = mb;
+        }
+    }
+
+    // bf16 form of consume().  The maximal entry still gets weight exactly 1
+    // (1.0 is a bf16 value), and an entry of weight 0 adds exactly 0, so a
+    // single-entry row returns its value exactly.  Steps with an odd number of
+    // valid entries pair the last one with a weight-0 copy.
+    __device__ __forceinline__ void consume_dot2(const Batch& bt, int nvalid, float c) {
+#pragma clang fp contract(off)
+        constexpr int U = Gm::kU;
+        float s[U][Gm::kNV];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int k = 0; k < Gm::kNV; ++k) {
+                const uint4 kr = bt.k[u][k], qr = qraw[k];
+                float d = dot2_bf16(qr.x, kr.x, 0.0f);
+                d = dot2_bf16(qr.y, kr.y, d);
+                d = dot2_bf16(qr.z, kr.z, d);
+                d = dot2_bf16(qr.w, kr.w, d);
+                d = head_sum<Gm::kHL>(d) * c;
+                s[u][k] = (u < nvalid) ? d : -INFINITY;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            float mb = m[k];
+#pragma unroll
+            for (int u = 0; u < U; ++u) mb = fmaxf(mb, s[u][k]);
+            const float corr = fast_exp2(m[k] - mb);  // 0 on the first step (m = -inf)
+            l[k] *= corr;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] *= corr;
+#pragma unroll
+            for (int u = 0; u < U; u += 2) {
+                const float p0 = fast_exp2(s[u][k] - mb), p1 = fast_exp2(s[u + 1][k] - mb);
+                l[k] += p0;  // the normaliser (and so lse) from the fp32 weights
+                l[k] += p1;
+                const uint32_t pp = pack_bf16(p0, p1);
+                const uint4 v0 = bt.v[u][k], v1 = bt.v[u + 1][k];
+                const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w}, a1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    acc[k][2 * x] = dot2_bf16(pp, pair_lo(a0[x], a1[x]), acc[k][2 * x]);
+                    acc[k][2 * x + 1] = dot2_bf16(pp, pair_hi(a0[x], a1[x]), acc[k][2 * x + 1]);
+                }
             }
             m[k] = mb;
         }

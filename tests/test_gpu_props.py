@@ -132,6 +132,43 @@ def test_offsets_beyond_4_gib():
     torch.cuda.empty_cache()
 
 
+def max_edge_graph():
+    """CSR with E = 2^31 - 1 entries, the largest count the boundary accepts.
+    Degrees cycle through every row class of the degree partition (empty,
+    light, the light/medium and medium/front boundaries, a front row in one
+    chunk, rows split into several and into the maximum number of chunks);
+    sources are uniform."""
+    cyc = np.array([0, 1, 5, 64, 65, 255, 256, 1024, 1025, 65000], dtype=np.int64)
+    e_max = (1 << 31) - 1
+    reps = e_max // int(cyc.sum())
+    deg = np.concatenate([np.tile(cyc, reps), [e_max - reps * int(cyc.sum())]])
+    rowptr = np.zeros(deg.size + 1, dtype=np.int64)
+    np.cumsum(deg, out=rowptr[1:])
+    colidx = np.random.default_rng(31).integers(0, deg.size, size=e_max, dtype=np.int32)
+    return rowptr, colidx
+
+
+def test_max_edge_count():
+    rowptr, colidx = max_edge_graph()
+    N, E = rowptr.size - 1, int(rowptr[-1])
+    assert E == (1 << 31) - 1
+    print("max-E graph: N", N, "E", E, flush=True)
+    H, D = 1, 32
+    Q, K, V = synth.features(31, N, H, D, "f32")
+    scale = np.float32(1 / math.sqrt(D))
+    got = run_gpu(rowptr, colidx, Q, K, V, scale)
+    rows = np.unique(np.concatenate([np.arange(40), np.arange(N - 40, N),
+                                     synth_rows(rowptr)]))
+    ref, absagg, _ = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, rows=rows, want_lse=False)
+    assert np.all(np.isfinite(got[rows]))
+    assert gate_error(got[rows], ref, absagg) <= TOL_F32
+
+
+def synth_rows(rowptr):
+    from tests.helpers import sample_rows
+    return sample_rows(rowptr, n_random=300, n_top=16)
+
+
 def test_csr_validator():
     rowptr, colidx = synth.ragged_graph(9, 500, max_deg=10)
     r, c = to_device(rowptr), to_device(colidx)
