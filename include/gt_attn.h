@@ -186,7 +186,9 @@ gt_status gt_gatv2_fwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* col
  * Layouts: Q, K, V, out, dout, dQ, dK, dV [N][H][D] in `dtype`, 16-byte
  * aligned; lse float [N][H].  Gradients are accumulated in fp32 and written
  * in `dtype` (bf16 rounded to nearest even); they must not overlap the
- * inputs or each other.  Asynchronous on `stream`; uses the stream's cached
+ * inputs or each other.  With bf16 features the two dot products per entry
+ * are bf16 dot products accumulated in fp32, and each entry's coefficients
+ * (ds and alpha) are rounded to bf16 before they multiply its vectors.  Asynchronous on `stream`; uses the stream's cached
  * workspace.
  */
 gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx,

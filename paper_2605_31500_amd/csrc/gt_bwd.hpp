@@ -48,12 +48,27 @@ struct BwdParams {
     float* part;  // [slot][NACC * H * D]
 };
 
+// bf16 dot over the four pairs of two 16-byte vectors, accumulated in fp32
+__device__ __forceinline__ float dot8_bf16(const uint4& a, const uint4& b) {
+    float d = dot2_bf16(a.x, b.x, 0.0f);
+    d = dot2_bf16(a.y, b.y, d);
+    d = dot2_bf16(a.z, b.z, d);
+    return dot2_bf16(a.w, b.w, d);
+}
+
 template <typename T, int H, int D, int MODE>
 struct BwdState {
     using Gm = Geo<T, H, D>;
     static constexpr int NV = Gm::kNV, EPV = Gm::kEPV, U = Gm::kU;
     static constexpr int NACC = MODE ? 2 : 1;
-    float a[NV][EPV], b[NV][EPV];
+    // bf16 features: the two dots per entry are bf16 dot2 on raw pairs, and
+    // the accumulations pair two entries: their coefficients (ds, alpha) are
+    // rounded to one bf16 pair and dot2 multiplies it with the two entries'
+    // elements, accumulating in fp32.
+    static constexpr bool kDot2 = std::is_same<T, bf16_tag>::value;
+    static_assert(!kDot2 || U % 2 == 0, "dot2 pairs entries");
+    float a[kDot2 ? 1 : NV][EPV], b[kDot2 ? 1 : NV][EPV];
+    uint4 araw[kDot2 ? NV : 1], braw[kDot2 ? NV : 1];
     float acc1[NV][EPV], acc2[NV][EPV];
     float L2[NV], Dl[NV];  // pass 0: the row's statistics (per vector slot's head)
 
@@ -61,8 +76,15 @@ struct BwdState {
         const int64_t off = row * (int64_t)Gm::kRowBytes + lig * 16;
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
-            widen<T>(*reinterpret_cast<const uint4*>(p.A + off + k * Gm::kG * 16), a[k]);
-            widen<T>(*reinterpret_cast<const uint4*>(p.B + off + k * Gm::kG * 16), b[k]);
+            const uint4 ar = *reinterpret_cast<const uint4*>(p.A + off + k * Gm::kG * 16);
+            const uint4 br = *reinterpret_cast<const uint4*>(p.B + off + k * Gm::kG * 16);
+            if constexpr (kDot2) {
+                araw[k] = ar;
+                braw[k] = br;
+            } else {
+                widen<T>(ar, a[k]);
+                widen<T>(br, b[k]);
+            }
 #pragma unroll
             for (int e = 0; e < EPV; ++e) acc1[k][e] = acc2[k][e] = 0.0f;
         }
@@ -70,11 +92,16 @@ struct BwdState {
 #pragma unroll
             for (int k = 0; k < NV; ++k) {
                 const int v = lig + k * Gm::kG, h = v / Gm::kHL;
-                float o[EPV];
-                widen<T>(*reinterpret_cast<const uint4*>(p.O + off + k * Gm::kG * 16), o);
+                const uint4 orw = *reinterpret_cast<const uint4*>(p.O + off + k * Gm::kG * 16);
                 float d = 0.0f;
+                if constexpr (kDot2) {
+                    d = dot8_bf16(orw, braw[k]);
+                } else {
+                    float o[EPV];
+                    widen<T>(orw, o);
 #pragma unroll
-                for (int e = 0; e < EPV; ++e) d = fmaf(o[e], b[k][e], d);
+                    for (int e = 0; e < EPV; ++e) d = fmaf(o[e], b[k][e], d);
+                }
                 Dl[k] = head_sum<Gm::kHL>(d);
                 L2[k] = p.lse[row * H + h] * 1.4426950408889634f;
                 if (v % Gm::kHL == 0) p.delta[row * H + h] = Dl[k];
@@ -99,6 +126,39 @@ struct BwdState {
                     dg[u][k] = p.delta[(int64_t)j[u] * H + h];
                 }
             }
+        }
+        if constexpr (kDot2) {
+#pragma unroll
+            for (int u = 0; u < U; u += 2) {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) {
+                    float al[2], ds[2];
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        const float sc = head_sum<Gm::kHL>(dot8_bf16(araw[k], xr[u + t][k])) * p.c;
+                        const float dd = head_sum<Gm::kHL>(dot8_bf16(braw[k], yr[u + t][k]));
+                        const float l2 = MODE == 1 ? lg[u + t][k] * 1.4426950408889634f : L2[k];
+                        const float dl = MODE == 1 ? dg[u + t][k] : Dl[k];
+                        al[t] = (u + t < nvalid) ? fast_exp2(sc - l2) : 0.0f;
+                        ds[t] = al[t] * (dd - dl);
+                    }
+                    const uint32_t pds = pack_bf16(ds[0], ds[1]);
+                    const uint32_t pal = pack_bf16(al[0], al[1]);
+                    const uint4 x0 = xr[u][k], x1 = xr[u + 1][k], y0 = yr[u][k], y1 = yr[u + 1][k];
+                    const uint32_t xa[4] = {x0.x, x0.y, x0.z, x0.w}, xb[4] = {x1.x, x1.y, x1.z, x1.w};
+                    const uint32_t ya[4] = {y0.x, y0.y, y0.z, y0.w}, yb[4] = {y1.x, y1.y, y1.z, y1.w};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc1[k][2 * q] = dot2_bf16(pds, pair_lo(xa[q], xb[q]), acc1[k][2 * q]);
+                        acc1[k][2 * q + 1] = dot2_bf16(pds, pair_hi(xa[q], xb[q]), acc1[k][2 * q + 1]);
+                        if constexpr (MODE == 1) {
+                            acc2[k][2 * q] = dot2_bf16(pal, pair_lo(ya[q], yb[q]), acc2[k][2 * q]);
+                            acc2[k][2 * q + 1] = dot2_bf16(pal, pair_hi(ya[q], yb[q]), acc2[k][2 * q + 1]);
+                        }
+                    }
+                }
+            }
+            return;
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
