@@ -477,7 +477,8 @@ def main() -> int:
                        **({"layer": "gatv2", "slope": GATV2_SLOPE} if args.gatv2 else {})),
         "roofline": {
             "bound": "hbm",
-            "kernel": "gt_attn_kernel" + (" (GATv2 score)" if args.gatv2 else ""),
+            "kernel": ("gt_tile_kernel + gt_attn_kernel" if args.dense_tiles else "gt_attn_kernel")
+                      + (" (GATv2 score)" if args.gatv2 else ""),
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",

@@ -270,8 +270,8 @@ const char* gt_last_error_message(void);
 /*
  * Kernel timing for benchmarking.  While enabled, every attention call
  * records HIP events on its stream around its three phases: [0] partition
- * (counter reset + degree binning), [1] the attention kernel, [2] the merge of
- * split rows.  gt_profile_collect waits for the recorded events, adds their
+ * (counter reset + degree binning), [1] the attention kernels (the dense-tile
+ * kernel, when enabled, and the CSR kernel), [2] the merge of split rows.  gt_profile_collect waits for the recorded events, adds their
  * elapsed milliseconds into ms[0..2], sets *calls, and clears the record.
  * Enabling or disabling also clears it.  Process-wide, thread-safe.
  */

@@ -1404,6 +1404,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
+    if (prof) (void)hipEventRecord(ev[1], stream);  // the attention phase includes the tile kernel
     if constexpr (kTileShape) {
         if (tiles) {
             TileParams tp;
@@ -1423,7 +1424,6 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
             if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "tile launch");
         }
     }
-    if (prof) (void)hipEventRecord(ev[1], stream);
 
     AttnParams ap;
     ap.rowptr = a.rowptr;
