@@ -220,6 +220,19 @@ template <int HL> __device__ __forceinline__ float head_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Streaming 16-byte accesses for data touched once per call (the row vector,
+// the output row): non-temporal, so they do not displace the gathered K/V rows
+// that other rows reuse from L2 and the Infinity Cache.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_once(const char* p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store_once(char* p, const uint4& x) {
+    const u32x4_t v = {x.x, x.y, x.z, x.w};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4_t*>(p));
+}
+
 // bf16 pair arithmetic (gfx950 v_dot2c_f32_bf16, v_cvt_pk_bf16_f32, v_perm_b32).
 // A dword holds bf16 element 2k in its low half and 2k+1 in its high half.
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -268,13 +281,15 @@ template <typename T, int H, int D, int KIND = KIND_GT>
 struct RowState {
     using Gm = Geo<T, H, D>;
     static constexpr bool kGat = KIND == KIND_GATV2;
-    // bf16 graph-transformer rows: scores with bf16 dot2 on the raw Q and K
-    // pairs, and P*V with the weights of two entries rounded to one bf16 pair
-    // and dot2 against the two entries' values: about half the vector
-    // instructions of widening every element to fp32.  The normaliser sums
-    // the fp32 weights, so lse keeps fp32 accuracy; the rounded weights then
-    // sum to within 2^-9 of it, which bounds the extra error of out by
-    // 2^-9 * sum_e p_e |v_e| / sum_e p_e.
+    // bf16 graph-transformer rows: scores are bf16 dot2 on the raw Q and K
+    // pairs, and P*V pairs two entries: their weights are rounded to one bf16
+    // pair and a dot2 multiplies it with the same element of the two entries'
+    // value rows (paired with v_perm), accumulating in fp32.  Against widening
+    // every element to fp32 this halves the vector instructions per entry.  The
+    // normaliser sums the fp32 weights, so lse keeps fp32 accuracy; the rounded
+    // weights sum to within 2^-9 of it, which bounds the extra error of out by
+    // 2^-9 * sum_e p_e |v_e| / sum_e p_e.  (GATv2 widens its gathered rows for
+    // the score anyway, and reusing them for P*V measured faster than pairs.)
     static constexpr bool kDot2 = std::is_same<T, bf16_tag>::value && !kGat;
     static_assert(!kDot2 || Gm::kU % 2 == 0, "dot2 pairs entries");
     float q[Gm::kNV][Gm::kEPV];
@@ -290,7 +305,7 @@ struct RowState {
         const char* qrow = Qb + row * (int64_t)Gm::kRowBytes + lig * 16;
 #pragma unroll
         for (int k = 0; k < Gm::kNV; ++k) {
-            const uint4 r = *reinterpret_cast<const uint4*>(qrow + k * Gm::kG * 16);
+            const uint4 r = load_once(qrow + k * Gm::kG * 16);
             if constexpr (kDot2)
                 qraw[k] = r;
             else
@@ -337,108 +352,95 @@ struct RowState {
         }
     }
 
+    // Value row of entry u in vector slot k (GATv2: the gathered R row).
+    __device__ __forceinline__ static const uint4& value(const Batch& bt, int u, int k) {
+        if constexpr (kGat)
+            return bt.k[u][k];
+        else
+            return bt.v[u][k];
+    }
+
+    // Score of entry u in vector slot k (log2 units, before masking).
+    __device__ __forceinline__ float score(const Batch& bt, int u, int k, float c) const {
+#pragma clang fp contract(off)
+        float d = 0.0f;
+        if constexpr (kDot2) {
+            const uint4 kr = bt.k[u][k], qr = qraw[k];
+            d = dot2_bf16(qr.x, kr.x, d);
+            d = dot2_bf16(qr.y, kr.y, d);
+            d = dot2_bf16(qr.z, kr.z, d);
+            d = dot2_bf16(qr.w, kr.w, d);
+        } else {
+            float kf[Gm::kEPV];
+            widen<T>(bt.k[u][k], kf);
+            if constexpr (kGat) {
+#pragma unroll
+                for (int e = 0; e < Gm::kEPV; ++e) {
+                    const float x = q[k][e] + kf[e];
+                    d = fmaf(a[k][e], x, d);
+                    d = fmaf(a2[k][e], fabsf(x), d);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < Gm::kEPV; ++e) d = fmaf(q[k][e], kf[e], d);
+            }
+        }
+        return head_sum<Gm::kHL>(d) * c;
+    }
+
     // Online-softmax update with the U entries of a batch; entries u >= nvalid
-    // are copies of valid indices and contribute nothing (score -inf).
+    // are copies of valid indices and contribute nothing (score -inf, weight 0).
+    // The maximal entry gets weight exactly 1 (also in bf16), and an entry of
+    // weight 0 adds exactly 0, so a single-entry row returns its value exactly;
+    // dot2 steps with an odd number of valid entries pair the last one with a
+    // weight-0 copy.
     __device__ __forceinline__ void consume(const Batch& bt, int nvalid, float c) {
         // No implicit contraction: fusing the score product into the later
         // subtraction of the running max would give the maximal entry a weight
         // of 2^(rounding error) instead of exactly 1.
 #pragma clang fp contract(off)
-        if constexpr (kDot2) {
-            consume_dot2(bt, nvalid, c);
-            return;
-        }
         constexpr int U = Gm::kU;
         float s[U][Gm::kNV];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+        for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int k = 0; k < Gm::kNV; ++k) {
-                float kf[Gm::kEPV];
-                widen<T>(bt.k[u][k], kf);
-                float d = 0.0f;
-                if constexpr (kGat) {
+                const float d = score(bt, u, k, c);  // unconditional: the head sum is cross-lane
+                s[u][k] = (u < nvalid) ? d : -INFINITY;
+            }
 #pragma unroll
-                    for (int e = 0; e < Gm::kEPV; ++e) {
-                        const float x = q[k][e] + kf[e];
-                        d = fmaf(a[k][e], x, d);
-                        d = fmaf(a2[k][e], fabsf(x), d);
+        for (int k = 0; k < Gm::kNV; ++k) {
+            float mb = m[k];
+#pragma unroll
+            for (int u = 0; u < U; ++u) mb = fmaxf(mb, s[u][k]);
+            const float corr = fast_exp2(m[k] - mb);  // 0 on the first step (m = -inf)
+            l[k] *= corr;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] *= corr;
+            if constexpr (kDot2) {
+#pragma unroll
+                for (int u = 0; u < U; u += 2) {
+                    const float p0 = fast_exp2(s[u][k] - mb), p1 = fast_exp2(s[u + 1][k] - mb);
+                    l[k] += p0;  // the normaliser (and so lse) from the fp32 weights
+                    l[k] += p1;
+                    const uint32_t pp = pack_bf16(p0, p1);
+                    const uint4 v0 = value(bt, u, k), v1 = value(bt, u + 1, k);
+                    const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w}, a1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+                    for (int x = 0; x < 4; ++x) {
+                        acc[k][2 * x] = dot2_bf16(pp, pair_lo(a0[x], a1[x]), acc[k][2 * x]);
+                        acc[k][2 * x + 1] = dot2_bf16(pp, pair_hi(a0[x], a1[x]), acc[k][2 * x + 1]);
                     }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < Gm::kEPV; ++e) d = fmaf(q[k][e], kf[e], d);
                 }
-                d = head_sum<Gm::kHL>(d) * c;
-                s[u][k] = (u < nvalid) ? d : -INFINITY;
-            }
-        }
+            } else {
 #pragma unroll
-        for (int k = 0; k < Gm::kNV; ++k) {
-            float mb = m[k];
+                for (int u = 0; u < U; ++u) {
+                    const float pu = fast_exp2(s[u][k] - mb);
+                    l[k] += pu;
+                    float vf[Gm::kEPV];
+                    widen<T>(value(bt, u, k), vf);
 #pragma unroll
-            for (int u = 0; u < U; ++u) mb = fmaxf(mb, s[u][k]);
-            const float corr = fast_exp2(m[k] - mb);  // 0 on the first step (m = -inf)
-            l[k] *= corr;
-#pragma unroll
-            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] *= corr;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const float pu = fast_exp2(s[u][k] - mb);
-                l[k] += pu;
-                float vf[Gm::kEPV];
-                if constexpr (kGat)
-                    widen<T>(bt.k[u][k], vf);
-                else
-                    widen<T>(bt.v[u][k], vf);
-#pragma unroll
-                for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = fmaf(pu, vf[e], acc[k][e]);
-            }
-            m[k] = mb;
-        }
-    }
-
-    // bf16 form of consume().  The maximal entry still gets weight exactly 1
-    // (1.0 is a bf16 value), and an entry of weight 0 adds exactly 0, so a
-    // single-entry row returns its value exactly.  Steps with an odd number of
-    // valid entries pair the last one with a weight-0 copy.
-    __device__ __forceinline__ void consume_dot2(const Batch& bt, int nvalid, float c) {
-#pragma clang fp contract(off)
-        constexpr int U = Gm::kU;
-        float s[U][Gm::kNV];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-#pragma unroll
-            for (int k = 0; k < Gm::kNV; ++k) {
-                const uint4 kr = bt.k[u][k], qr = qraw[k];
-                float d = dot2_bf16(qr.x, kr.x, 0.0f);
-                d = dot2_bf16(qr.y, kr.y, d);
-                d = dot2_bf16(qr.z, kr.z, d);
-                d = dot2_bf16(qr.w, kr.w, d);
-                d = head_sum<Gm::kHL>(d) * c;
-                s[u][k] = (u < nvalid) ? d : -INFINITY;
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < Gm::kNV; ++k) {
-            float mb = m[k];
-#pragma unroll
-            for (int u = 0; u < U; ++u) mb = fmaxf(mb, s[u][k]);
-            const float corr = fast_exp2(m[k] - mb);  // 0 on the first step (m = -inf)
-            l[k] *= corr;
-#pragma unroll
-            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] *= corr;
-#pragma unroll
-            for (int u = 0; u < U; u += 2) {
-                const float p0 = fast_exp2(s[u][k] - mb), p1 = fast_exp2(s[u + 1][k] - mb);
-                l[k] += p0;  // the normaliser (and so lse) from the fp32 weights
-                l[k] += p1;
-                const uint32_t pp = pack_bf16(p0, p1);
-                const uint4 v0 = bt.v[u][k], v1 = bt.v[u + 1][k];
-                const uint32_t a0[4] = {v0.x, v0.y, v0.z, v0.w}, a1[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-                for (int x = 0; x < 4; ++x) {
-                    acc[k][2 * x] = dot2_bf16(pp, pair_lo(a0[x], a1[x]), acc[k][2 * x]);
-                    acc[k][2 * x + 1] = dot2_bf16(pp, pair_hi(a0[x], a1[x]), acc[k][2 * x + 1]);
+                    for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = fmaf(pu, vf[e], acc[k][e]);
                 }
             }
             m[k] = mb;
@@ -482,7 +484,7 @@ struct RowState {
             float o[Gm::kEPV];
 #pragma unroll
             for (int e = 0; e < Gm::kEPV; ++e) o[e] = acc[k][e] * inv;
-            *reinterpret_cast<uint4*>(orow + k * Gm::kG * 16) = narrow<T>(o);
+            store_once(orow + k * Gm::kG * 16, narrow<T>(o));
             const int v = lig + k * Gm::kG;
             if (lse && v % Gm::kHL == 0) lse[row * H + v / Gm::kHL] = lse_of(m[k], l[k]);
         }
@@ -546,21 +548,39 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
 // loaded before the current row's work starts, and its first index tile is
 // loaded while the current row's first K/V batch is in flight, so a short row
 // costs about one memory latency instead of three (rowptr -> colidx -> K/V).
+// An index tile holds LightTile<G>::kR * G entries (kR loads per lane).
+template <int G> struct LightTile {
+    static constexpr int kR = G >= 64 ? 1 : 2;
+    static constexpr int kEntries = kR * G;
+};
+
 template <typename T, int H, int D, int KIND>
 __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int64_t it_end,
                                            int64_t stride, int g, int lig,
                                            int32_t* __restrict__ gtile) {
     using Gm = Geo<T, H, D>;
     constexpr int U = Gm::kU, G = Gm::kG, P = Gm::kP;
+    constexpr int R = LightTile<G>::kR, TE = LightTile<G>::kEntries;
+    // entries [tb, tb + TE) of a row ending at ce (clamped to its last entry)
+    auto load_tile = [&](int64_t tb, int64_t ce, int32_t (&v)[R]) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t pos = tb + r * G + lig;
+            v[r] = p.colidx[pos < ce ? pos : ce - 1];
+        }
+    };
     int64_t row = it * P + g;
     bool ok = it < it_end && row < p.N;
     int64_t b = ok ? p.rowptr[row] : 0, e = ok ? p.rowptr[row + 1] : 0;
     bool mine = ok && (e - b) <= p.light_max;
-    int32_t idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
+    int32_t idx[R] = {};
+    if (mine && e > b) load_tile(b, e, idx);
     while (it < it_end) {
         const int64_t crow = row, cb = b, ce = e;
         const bool cmine = mine;
-        const int32_t cidx = idx;
+        int32_t tv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) tv[r] = idx[r];
         it += stride;
         row = it * P + g;
         ok = it < it_end && row < p.N;
@@ -571,13 +591,13 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
         if (cmine) {
             RowState<T, H, D, KIND> st;
             st.begin(p.Q, crow, lig, p.att, p.slope);
-            for (int64_t tb = cb; tb < ce; tb += G) {
-                int32_t tile_idx = cidx;
-                if (tb != cb) tile_idx = p.colidx[(tb + lig < ce) ? tb + lig : ce - 1];
+            for (int64_t tb = cb; tb < ce; tb += TE) {
+                if (tb != cb) load_tile(tb, ce, tv);
                 wave_lds_fence();
-                gtile[lig] = tile_idx;
+#pragma unroll
+                for (int r = 0; r < R; ++r) gtile[r * G + lig] = tv[r];
                 wave_lds_fence();
-                const int nt = (int)((ce - tb) < G ? (ce - tb) : G);
+                const int nt = (int)((ce - tb) < TE ? (ce - tb) : TE);
                 for (int t = 0; t < nt; t += U) {
                     const int nvalid = nt - t < U ? nt - t : U;
                     int32_t j[U];
@@ -586,7 +606,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
                     typename RowState<T, H, D, KIND>::Batch bt;
                     st.issue(p.K, p.V, j, lig, bt);
                     if (!fetched) {  // next row's first tile, overlapped with this batch
-                        idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
+                        if (mine && e > b) load_tile(b, e, idx);
                         fetched = true;
                     }
                     st.consume(bt, nvalid, p.c);
@@ -594,7 +614,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
             }
             st.store_out(p.out, p.lse, crow, lig);
         }
-        if (!fetched) idx = (mine && e > b) ? p.colidx[(b + lig < e) ? b + lig : e - 1] : 0;
+        if (!fetched && mine && e > b) load_tile(b, e, idx);
     }
 }
 
@@ -604,7 +624,9 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
 template <typename T, int H, int D, int KIND>
 __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     using Gm = Geo<T, H, D>;
-    __shared__ int32_t tiles[kWavesPerBlock][kWave];
+    // per wave: one 64-entry tile (wave items) or P light-row tiles
+    constexpr int kTileWords = Gm::kP * LightTile<Gm::kG>::kEntries > kWave ? Gm::kP * LightTile<Gm::kG>::kEntries : kWave;
+    __shared__ int32_t tiles[kWavesPerBlock][kTileWords];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
     int32_t* tile = tiles[wv];
@@ -631,7 +653,8 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
     const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
     const int g = lane / Gm::kG, lig = lane % Gm::kG;
-    if (!p.skip_light) light_rows<T, H, D, KIND>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * Gm::kG);
+    if (!p.skip_light) light_rows<T, H, D, KIND>(p, lo + lw, hi, waves_per_xcd, g, lig,
+                                                  tile + g * LightTile<Gm::kG>::kEntries);
 }
 
 // ------------------------------------------------------- dense-tile path

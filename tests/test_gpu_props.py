@@ -132,6 +132,19 @@ def test_offsets_beyond_4_gib():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("mode", ["group_per_row", "wave_per_row"])
+def test_degree_agnostic_mappings(mode):
+    """The degree-agnostic tunings timed by the allocation ablation (every row
+    on one lane group, or on one wavefront, with no split) compute the same
+    function: parity on the power-law workload, whose hub rows then run whole
+    on one group or one wave."""
+    import bench
+    w = synth.config(1)
+    got = run_gpu(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, tuning=bench.ABLATION_MODES[mode])
+    ref, absagg, _ = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_lse=False)
+    assert gate_error(got, ref, absagg) <= TOL_F32
+
+
 def max_edge_graph():
     """CSR with E = 2^31 - 1 entries, the largest count the boundary accepts.
     Degrees cycle through every row class of the degree partition (empty,
