@@ -36,6 +36,7 @@
 #include <hip/hip_runtime.h>
 
 #include <array>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -1211,6 +1212,43 @@ Profiler& profiler() {
     return *p;
 }
 
+// The four phase events of one profiled call (when profiling is enabled):
+// created by start(), recorded by mark(), handed to the profiler by commit().
+// A call that fails before commit() destroys them.
+struct PhaseEvents {
+    std::array<hipEvent_t, 4> ev{};
+    bool on = false;
+    hipError_t start(hipStream_t stream) {
+        Profiler& pr = profiler();
+        {
+            std::lock_guard<std::mutex> lk(pr.mu);
+            on = pr.on;
+        }
+        if (!on) return hipSuccess;
+        for (auto& e : ev) {
+            const hipError_t he = hipEventCreate(&e);
+            if (he != hipSuccess) return he;
+        }
+        return hipEventRecord(ev[0], stream);
+    }
+    void mark(int k, hipStream_t stream) {
+        if (on) (void)hipEventRecord(ev[k], stream);
+    }
+    void commit(hipStream_t stream) {
+        if (!on) return;
+        (void)hipEventRecord(ev[3], stream);
+        Profiler& pr = profiler();
+        std::lock_guard<std::mutex> lk(pr.mu);
+        pr.pending.push_back(ev);
+        on = false;
+    }
+    ~PhaseEvents() {
+        if (on)
+            for (auto e : ev)
+                if (e) (void)hipEventDestroy(e);
+    }
+};
+
 // Workspace cache: one buffer per (device, stream) -- per thread for the
 // per-thread default stream -- reused by every later call on that stream, so
 // steady-state calls allocate nothing and stream order keeps reuse safe.  The
@@ -1290,7 +1328,7 @@ PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
 }
 
 int device_cus(int dev) {
-    static int cache[64] = {0};
+    static std::atomic<int> cache[64];
     if (dev < 0 || dev >= 64) return 256;
     if (cache[dev] == 0) {
         int n = 0;
@@ -1302,7 +1340,7 @@ int device_cus(int dev) {
 
 template <typename T, int H, int D, int KIND>
 int attn_blocks_per_cu(int dev) {
-    static int cache[64] = {0};
+    static std::atomic<int> cache[64];
     if (dev < 0 || dev >= 64) return 4;
     if (cache[dev] == 0) {
         int nb = 0;
@@ -1400,18 +1438,8 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     // next call cannot rely on its counters; a failed launch leaves this false.
     we.counters_zero = false;
 
-    Profiler& pr = profiler();
-    bool prof;
-    {
-        std::lock_guard<std::mutex> lk(pr.mu);
-        prof = pr.on;
-    }
-    std::array<hipEvent_t, 4> ev{};
-    if (prof) {
-        for (auto& e : ev)
-            if ((he = hipEventCreate(&e)) != hipSuccess) return hip_fail(he, "hipEventCreate");
-        (void)hipEventRecord(ev[0], stream);
-    }
+    PhaseEvents ph;
+    if ((he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
 
     PartParams pp;
     pp.rowptr = a.rowptr;
@@ -1427,7 +1455,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
-    if (prof) (void)hipEventRecord(ev[1], stream);  // the attention phase includes the tile kernel
+    ph.mark(1, stream);  // the attention phase includes the tile kernel
     if constexpr (kTileShape) {
         if (tiles) {
             TileParams tp;
@@ -1471,7 +1499,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.skip_light = tiles ? 1 : 0;
     hipLaunchKernelGGL((gt_attn_kernel<T, H, D, KIND>), dim3(grid), dim3(kBlock), 0, stream, ap);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "attention launch");
-    if (prof) (void)hipEventRecord(ev[2], stream);
+    ph.mark(2, stream);
 
     MergeParams mp;
     mp.cap_heavy = (int32_t)caps.heavy;
@@ -1487,11 +1515,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     if (merge_grid < 1) merge_grid = 1;
     hipLaunchKernelGGL((gt_merge_kernel<T, H, D>), dim3(merge_grid), dim3(kBlock), 0, stream, mp);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "merge launch");
-    if (prof) {
-        (void)hipEventRecord(ev[3], stream);
-        std::lock_guard<std::mutex> lk(pr.mu);
-        pr.pending.push_back(ev);
-    }
+    ph.commit(stream);
     we.parity = 1 - we.parity;
     we.counters_zero = true;
     return GT_SUCCESS;

@@ -357,7 +357,7 @@ struct ReduceArgs {
 
 template <typename T, int NVEC>
 int reduce_blocks_per_cu(int dev) {
-    static int cache[64] = {0};
+    static std::atomic<int> cache[64];
     if (dev < 0 || dev >= 64) return 4;
     if (cache[dev] == 0) {
         int nb = 0;
@@ -435,18 +435,8 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     int32_t* next_counters = cnt_sets + (1 - we.parity) * kCntSetWords;
     we.counters_zero = false;
 
-    Profiler& pr = profiler();
-    bool prof;
-    {
-        std::lock_guard<std::mutex> lk(pr.mu);
-        prof = pr.on;
-    }
-    std::array<hipEvent_t, 4> ev{};
-    if (prof) {
-        for (auto& e : ev)
-            if ((he = hipEventCreate(&e)) != hipSuccess) return hip_fail(he, "hipEventCreate");
-        (void)hipEventRecord(ev[0], stream);
-    }
+    PhaseEvents ph;
+    if ((he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
 
     PartParams pp;
     pp.rowptr = a.rowptr;
@@ -462,7 +452,7 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
-    if (prof) (void)hipEventRecord(ev[1], stream);
+    ph.mark(1, stream);
 
     ReduceParams rp;
     rp.rowptr = a.rowptr;
@@ -483,18 +473,14 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     rp.heavy = pp.heavy;
     hipLaunchKernelGGL((gt_reduce_kernel<T, NVEC>), dim3(grid), dim3(kBlock), 0, stream, rp);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "reduce launch");
-    if (prof) (void)hipEventRecord(ev[2], stream);
+    ph.mark(2, stream);
 
     int merge_grid = (int)((caps.heavy + kWavesPerBlock - 1) / kWavesPerBlock);
     if (merge_grid > device_cus(dev) * 8) merge_grid = device_cus(dev) * 8;
     if (merge_grid < 1) merge_grid = 1;
     hipLaunchKernelGGL((gt_reduce_merge_kernel<T, NVEC>), dim3(merge_grid), dim3(kBlock), 0, stream, rp);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "reduce merge launch");
-    if (prof) {
-        (void)hipEventRecord(ev[3], stream);
-        std::lock_guard<std::mutex> lk(pr.mu);
-        pr.pending.push_back(ev);
-    }
+    ph.commit(stream);
     we.parity = 1 - we.parity;
     we.counters_zero = true;
     return GT_SUCCESS;
