@@ -96,6 +96,11 @@ def _ptr(t):
 
 
 def _stream(device, stream):
+    """The HIP stream to launch on; the library launches on the current device,
+    so the tensors must live there."""
+    if device.index is not None and device.index != torch.cuda.current_device():
+        raise ValueError("tensors are on %s but the current device is cuda:%d; call under "
+                         "torch.cuda.device(%s)" % (device, torch.cuda.current_device(), device))
     if stream is None:
         stream = torch.cuda.current_stream(device)
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
@@ -110,6 +115,8 @@ def _check_tensors(rowptr, colidx, Q, K, V, out, dtypes):
             raise ValueError(name + " must be a device tensor")
         if not t.is_contiguous():
             raise ValueError(name + " must be contiguous")
+    if any(t.device != Q.device for t in (rowptr, colidx, K, V, out)):
+        raise ValueError("all tensors must be on one device")
     if rowptr.dtype != torch.int64 or colidx.dtype != torch.int32:
         raise TypeError("rowptr must be int64 and colidx int32")
     if Q.dim() != 3 or K.shape != Q.shape or V.shape != Q.shape or out.shape != Q.shape:
@@ -152,8 +159,8 @@ def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None
         tuning = GtTuning(**tuning)
     tp = ctypes.byref(tuning) if tuning is not None else None
     if lse is not None:
-        if not (lse.is_cuda and lse.is_contiguous() and lse.dtype == torch.float32
-                and tuple(lse.shape) == (N, H)):
+        if not (lse.is_cuda and lse.device == out.device and lse.is_contiguous()
+                and lse.dtype == torch.float32 and tuple(lse.shape) == (N, H)):
             raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
     _check(load_library().gt_attn_fwd_ex(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
                                          _ptr(V), _ptr(out), _ptr(lse), N, colidx.numel(), H, D,
@@ -170,15 +177,15 @@ def gt_gatv2_fwd(rowptr, colidx, L, R, att, slope, out, tuning=None, stream=None
         dtype, allowed = GT_DTYPE_BF16, (torch.bfloat16, torch.int16, torch.uint16)
     _check_tensors(rowptr, colidx, L, R, R, out, allowed)
     N, H, D = L.shape
-    if not (isinstance(att, torch.Tensor) and att.is_cuda and att.is_contiguous()
+    if not (isinstance(att, torch.Tensor) and att.device == L.device and att.is_contiguous()
             and att.dtype == torch.float32 and tuple(att.shape) == (H, D)):
         raise ValueError("att must be a contiguous float32 [H, D] device tensor")
     if isinstance(tuning, dict):
         tuning = GtTuning(**tuning)
     tp = ctypes.byref(tuning) if tuning is not None else None
     if lse is not None:
-        if not (lse.is_cuda and lse.is_contiguous() and lse.dtype == torch.float32
-                and tuple(lse.shape) == (N, H)):
+        if not (lse.is_cuda and lse.device == out.device and lse.is_contiguous()
+                and lse.dtype == torch.float32 and tuple(lse.shape) == (N, H)):
             raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
     _check(load_library().gt_gatv2_fwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(L), _ptr(R),
                                        _ptr(att), float(slope), _ptr(out), _ptr(lse), N,
@@ -194,6 +201,8 @@ def gt_dot_aggr(rowptr, colidx, X, out, mapping="feature", load_bytes=16, stream
     for name, t in (("rowptr", rowptr), ("colidx", colidx), ("X", X), ("out", out)):
         if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
             raise ValueError(name + " must be a contiguous device tensor")
+    if any(t.device != X.device for t in (rowptr, colidx, out)):
+        raise ValueError("all tensors must be on one device")
     if X.dtype != torch.float32 or out.dtype != torch.float32 or X.dim() != 2:
         raise TypeError("X must be float32 [N, F] and out float32 [N]")
     N, F = X.shape
@@ -218,6 +227,8 @@ def gt_segment_reduce(rowptr, colidx, X, out, arg=None, op="min", tuning=None, s
     for name, t in (("rowptr", rowptr), ("colidx", colidx), ("X", X), ("out", out)):
         if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
             raise ValueError(name + " must be a contiguous device tensor")
+    if any(t.device != X.device for t in (rowptr, colidx, out) + (() if arg is None else (arg,))):
+        raise ValueError("all tensors must be on one device")
     if rowptr.dtype != torch.int64 or colidx.dtype != torch.int32:
         raise TypeError("rowptr must be int64 and colidx int32")
     if X.dim() != 2 or out.shape != X.shape or X.dtype not in allowed or out.dtype != X.dtype:
@@ -249,8 +260,10 @@ def gt_attn_bwd(rowptr, colidx, rowptr_t, colidx_t, Q, K, V, out, dout, lse, dQ,
     N, H, D = Q.shape
     if colidx_t.numel() != colidx.numel():
         raise ValueError("the transposed structure must have as many entries as the CSR")
-    if not (lse.is_cuda and lse.is_contiguous() and lse.dtype == torch.float32
-            and tuple(lse.shape) == (N, H)):
+    if dout.device != Q.device:
+        raise ValueError("all tensors must be on one device")
+    if not (lse.is_cuda and lse.device == Q.device and lse.is_contiguous()
+            and lse.dtype == torch.float32 and tuple(lse.shape) == (N, H)):
         raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
     _check(load_library().gt_attn_bwd(dtype, _ptr(rowptr), _ptr(colidx), _ptr(rowptr_t),
                                       _ptr(colidx_t), _ptr(Q), _ptr(K), _ptr(V), _ptr(out),

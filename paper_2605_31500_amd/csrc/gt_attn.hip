@@ -1738,16 +1738,21 @@ gt_status gt_csr_validate(const int64_t* rowptr, const int32_t* colidx, int64_t 
     int32_t* bad = nullptr;
     hipError_t he = hipMallocAsync(reinterpret_cast<void**>(&bad), sizeof(int32_t), stream);
     if (he != hipSuccess) return fail(GT_ERROR_OUT_OF_MEMORY, "flag allocation failed");
-    if ((he = hipMemsetAsync(bad, 0, sizeof(int32_t), stream)) != hipSuccess) return hip_fail(he, "hipMemsetAsync");
+    // the flag is freed (stream-ordered) on every path once it was allocated
+    auto failed = [&](hipError_t e, const char* what) {
+        (void)hipFreeAsync(bad, stream);
+        return hip_fail(e, what);
+    };
+    if ((he = hipMemsetAsync(bad, 0, sizeof(int32_t), stream)) != hipSuccess) return failed(he, "hipMemsetAsync");
     const int64_t work = N > E ? N : E;
     int grid = (int)((work + kBlock - 1) / kBlock);
     if (grid > 4096) grid = 4096;
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(gt_csr_check_kernel, dim3(grid), dim3(kBlock), 0, stream, rowptr, colidx, N, E, bad);
-    if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "validate launch");
+    if ((he = hipGetLastError()) != hipSuccess) return failed(he, "validate launch");
     int32_t h_bad = 1;
     if ((he = hipMemcpyAsync(&h_bad, bad, sizeof(int32_t), hipMemcpyDeviceToHost, stream)) != hipSuccess)
-        return hip_fail(he, "hipMemcpyAsync");
+        return failed(he, "hipMemcpyAsync");
     (void)hipFreeAsync(bad, stream);
     if ((he = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(he, "hipStreamSynchronize");
     *valid = h_bad == 0 ? 1 : 0;
