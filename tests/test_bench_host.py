@@ -1,0 +1,78 @@
+"""Host-side logic of bench.py: the byte models, the counter bookkeeping and
+the one-GPU guard (no GPU needed)."""
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+
+import bench
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_model_bytes_match_the_per_edge_formula():
+    w = synth.config(0)
+    R = w.H * w.D * 4
+    want = 8 * (w.N + 1) + 4 * w.E + w.N * R + 2 * w.E * R + w.N * R
+    assert bench.model_bytes(w) == want
+    # GATv2 gathers one row per entry and reads the [H, D] fp32 attention vector
+    assert bench.gatv2_model_bytes(w) == want - w.E * R + 4 * w.H * w.D
+    assert bench.compulsory_bytes(w) == 8 * (w.N + 1) + 4 * w.E + 4 * w.N * R
+
+
+def test_reduce_model_bytes():
+    assert bench.reduce_model_bytes(10, 40, 16, 4) == 8 * 11 + 4 * 40 + 40 * 64 + 10 * 64 + 10 * 64
+
+
+def test_source_hash_covers_every_hip_source(tmp_path, monkeypatch):
+    h0 = bench.source_hash()
+    assert len(h0) == 16 and h0 == bench.source_hash()
+    d = tmp_path / "csrc"
+    d.mkdir()
+    (d / "a.hip").write_text("x")
+    (d / "b.hpp").write_text("y")
+    monkeypatch.setattr(bench, "KERNEL_SRC_DIR", str(d))
+    h1 = bench.source_hash()
+    (d / "b.hpp").write_text("z")  # a change in an included header changes the hash
+    assert bench.source_hash() != h1
+    (d / "notes.txt").write_text("ignored")
+    h2 = bench.source_hash()
+    (d / "notes.txt").write_text("still ignored")
+    assert bench.source_hash() == h2
+
+
+def test_stored_traffic_only_for_the_current_sources(tmp_path, monkeypatch):
+    f = tmp_path / "traffic.json"
+    f.write_text(json.dumps({"w": {"kernel_source_sha256_16": bench.source_hash(),
+                                   "hbm_bytes_per_launch": 123},
+                             "old": {"kernel_source_sha256_16": "0" * 16,
+                                     "hbm_bytes_per_launch": 456}}))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    assert bench.stored_traffic("w") == 123
+    assert bench.stored_traffic("old") is None
+    assert bench.stored_traffic("missing") is None
+
+
+def test_committed_traffic_entries_are_well_formed():
+    rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
+    for key, e in rec.items():
+        # each figure is a scaled counter truncated to whole bytes
+        assert abs(e["hbm_bytes_per_launch"] - e["fetch_bytes_per_launch"] - e["write_bytes_per_launch"]) <= 1
+        assert os.path.exists(os.path.join(ROOT, "profiles", e["summary"])), key
+
+
+def test_ablation_modes_keep_heavy_above_light():
+    for mode, tu in bench.ABLATION_MODES.items():
+        if tu:
+            assert tu["heavy_min_deg"] > tu["light_max_deg"] > 0, mode
+            assert max(tu.values()) < 2 ** 31
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
