@@ -726,7 +726,7 @@ struct TileLds {
             uint16_t k[kWin][KST];
             uint16_t vt[HD][kVtStride];
         } kv;
-        float acc[kWavesPerBlock][16][HD];
+        float acc[kWavesPerBlock][16][HD + 4];  // padded: the MFMA-layout writes hit distinct banks
     } big;
     float2 ml[kWavesPerBlock][16][H];
     int32_t ctile[kWavesPerBlock][kWave / (H * D / 8) * kWinMaxDeg];  // per lane group: one row's entries
@@ -749,20 +749,26 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
     // ---- 1. staging
     if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
     for (int v = tid; v < kWin * (HD / 8); v += kBlock) {
-        // consecutive lanes take consecutive rows, so the transposed 2-byte
-        // writes of a wave land in consecutive LDS addresses
+        // K rows as they are: 16 bytes of one row per lane
         const int cc = v % kWin, e0 = (v / kWin) * 8;
-        uint4 kx = make_uint4(0, 0, 0, 0), vx = make_uint4(0, 0, 0, 0);
-        if (r0 + cc < p.N) {
-            kx = *reinterpret_cast<const uint4*>(p.K + ((r0 + cc) * HD + e0) * 2);
-            vx = *reinterpret_cast<const uint4*>(p.V + ((r0 + cc) * HD + e0) * 2);
-        }
+        uint4 kx = make_uint4(0, 0, 0, 0);
+        if (r0 + cc < p.N) kx = *reinterpret_cast<const uint4*>(p.K + ((r0 + cc) * HD + e0) * 2);
         *reinterpret_cast<uint4*>(&lds.big.kv.k[cc][e0]) = kx;
-        const uint32_t w4[4] = {vx.x, vx.y, vx.z, vx.w};
+    }
+    for (int v = tid; v < (kWin / 2) * (HD / 8); v += kBlock) {
+        // V transposed: a lane takes 8 elements of two consecutive rows and writes
+        // each element pair as one dword, so the 32 lanes of a row pair write 32
+        // consecutive dwords of one vt row
+        const int pc = v % (kWin / 2), e0 = (v / (kWin / 2)) * 8;
+        const int64_t ra = r0 + 2 * pc;
+        uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
+        if (ra < p.N) va = *reinterpret_cast<const uint4*>(p.V + (ra * HD + e0) * 2);
+        if (ra + 1 < p.N) vb = *reinterpret_cast<const uint4*>(p.V + ((ra + 1) * HD + e0) * 2);
+        const uint32_t wa[4] = {va.x, va.y, va.z, va.w}, wb[4] = {vb.x, vb.y, vb.z, vb.w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            lds.big.kv.vt[e0 + 2 * q][cc] = (uint16_t)(w4[q] & 0xFFFFu);
-            lds.big.kv.vt[e0 + 2 * q + 1][cc] = (uint16_t)(w4[q] >> 16);
+            *reinterpret_cast<uint32_t*>(&lds.big.kv.vt[e0 + 2 * q][2 * pc]) = pair_lo(wa[q], wb[q]);
+            *reinterpret_cast<uint32_t*>(&lds.big.kv.vt[e0 + 2 * q + 1][2 * pc]) = pair_hi(wa[q], wb[q]);
         }
     }
     // this lane's strip row of Q (all heads), as MFMA B operands
