@@ -290,7 +290,8 @@ def run_backward(args, w, gt, torch, to_device, synth) -> dict:
         "data": "synthetic", "config": w.describe(),
         "roofline": {"bound": "hbm", "kernel": "gt_attn_bwd (whole call: 2 passes)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": stored_traffic(w.name + ":backward"),
                      "algorithmic_bytes_per_launch": mbytes, "kernel_ms": round(ms, 5)},
     }
 
