@@ -48,8 +48,9 @@
  * failures return a gt_status and set a thread-local message readable with
  * gt_last_error_message().  Validation never reads device memory.
  *
- * Supported shapes: H in {1, 2, 4, 8}, D in {32, 64, 128}; 0 <= E < 2^31;
- * 0 <= N < 2^31.
+ * Supported shapes: H in {1, 2, 4, 8} with D in {32, 64, 128, 256}, and for
+ * bf16 features also D = 512 with H in {1, 2, 4} (one head's D elements must
+ * fit 64 lanes of 16 bytes); 0 <= E < 2^31; 0 <= N < 2^31.
  */
 #ifndef GT_ATTN_H
 #define GT_ATTN_H

@@ -1537,6 +1537,10 @@ LaunchFn pick_hd(int32_t H, int32_t D) {
     GT_CASE(2, 32) GT_CASE(2, 64) GT_CASE(2, 128)
     GT_CASE(4, 32) GT_CASE(4, 64) GT_CASE(4, 128)
     GT_CASE(8, 32) GT_CASE(8, 64) GT_CASE(8, 128)
+    GT_CASE(1, 256) GT_CASE(2, 256) GT_CASE(4, 256) GT_CASE(8, 256)
+    if constexpr (std::is_same<T, bf16_tag>::value) {  // a head must fit 64 lanes of 16 bytes
+        GT_CASE(1, 512) GT_CASE(2, 512) GT_CASE(4, 512)
+    }
 #undef GT_CASE
     return nullptr;
 }
@@ -1561,7 +1565,7 @@ gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t st
         fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GT>(a.H, a.D) : pick_hd<bf16_tag, KIND_GT>(a.H, a.D);
     if (!fn)
         return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +
-                                                std::to_string(a.D) + "); H in {1,2,4,8}, D in {32,64,128}");
+                                                std::to_string(a.D) + "); H in {1,2,4,8} with D in {32,64,128,256}, or bf16 D = 512 with H in {1,2,4}");
     if (a.N == 0) return GT_SUCCESS;
     if (!a.rowptr) return fail(GT_ERROR_INVALID_VALUE, "rowptr is null");
     if (a.E > 0 && !a.colidx) return fail(GT_ERROR_INVALID_VALUE, "colidx is null");
@@ -1600,7 +1604,7 @@ gt_status run_bwd(gt_dtype dtype, const BwdArgs& a, hipStream_t stream) {
     BwdFn fn = dtype == GT_DTYPE_F32 ? pick_bwd<float>(a.H, a.D) : pick_bwd<bf16_tag>(a.H, a.D);
     if (!fn)
         return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +
-                                                std::to_string(a.D) + "); H in {1,2,4,8}, D in {32,64,128}");
+                                                std::to_string(a.D) + "); H in {1,2,4,8} with D in {32,64,128,256}, or bf16 D = 512 with H in {1,2,4}");
     if (a.N == 0) return GT_SUCCESS;
     if (!a.rowptr || !a.rowptr_t) return fail(GT_ERROR_INVALID_VALUE, "rowptr or rowptr_t is null");
     if (a.E > 0 && (!a.colidx || !a.colidx_t)) return fail(GT_ERROR_INVALID_VALUE, "colidx or colidx_t is null");

@@ -512,6 +512,10 @@ BwdFn pick_bwd(int32_t H, int32_t D) {
     GT_CASE(2, 32) GT_CASE(2, 64) GT_CASE(2, 128)
     GT_CASE(4, 32) GT_CASE(4, 64) GT_CASE(4, 128)
     GT_CASE(8, 32) GT_CASE(8, 64) GT_CASE(8, 128)
+    GT_CASE(1, 256) GT_CASE(2, 256) GT_CASE(4, 256) GT_CASE(8, 256)
+    if constexpr (std::is_same<T, bf16_tag>::value) {  // a head must fit 64 lanes of 16 bytes
+        GT_CASE(1, 512) GT_CASE(2, 512) GT_CASE(4, 512)
+    }
 #undef GT_CASE
     return nullptr;
 }

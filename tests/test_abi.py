@@ -49,7 +49,8 @@ def call(lib, dtype=0, rowptr=FAKE, colidx=FAKE, Q=FAKE, K=FAKE + 0x100000, V=FA
 
 
 @pytest.mark.parametrize("kw,status", [
-    (dict(H=3), 2), (dict(D=48), 2), (dict(D=256), 2), (dict(dtype=7), 2),
+    (dict(H=3), 2), (dict(D=48), 2), (dict(D=512), 2), (dict(D=1024, dtype=1), 2),
+    (dict(H=8, D=512, dtype=1), 2), (dict(dtype=7), 2),
     (dict(N=-1), 1), (dict(E=-5), 1), (dict(E=1 << 31), 1), (dict(N=1 << 31), 1),
     (dict(H=0), 1), (dict(scale=float("inf")), 1), (dict(scale=float("nan")), 1),
     (dict(rowptr=0), 1), (dict(colidx=0), 1), (dict(Q=0), 1), (dict(out=0), 1),

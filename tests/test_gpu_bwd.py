@@ -14,7 +14,9 @@ from tests.helpers import (TOL_BF16, TOL_F32, gate_error, run_gpu_fwd_bwd, sampl
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(h, d) for h in (1, 2, 4, 8) for d in (32, 64, 128)]
+SHAPES = [(h, d) for h in (1, 2, 4, 8) for d in (32, 64, 128, 256)]
+BF16_ONLY = [(1, 512), (2, 512), (4, 512)]  # a 512-element fp32 head exceeds 64 lanes of 16 B
+CASES = [(h, d, t) for (h, d) in SHAPES for t in ("f32", "bf16")] + [(h, d, "bf16") for (h, d) in BF16_ONLY]
 FORCED_SPLIT = {"light_max_deg": 2, "heavy_min_deg": 6, "chunk_edges": 64, "grid_blocks": 0}
 
 
@@ -45,8 +47,7 @@ def check_grads(rowptr, colidx, Q, K, V, dO, scale, got, dtype, rows=None, cols=
 
 
 @pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("H,D", SHAPES)
+@pytest.mark.parametrize("H,D,dtype", CASES)
 def test_lse_and_backward_small(H, D, dtype, split):
     N = 300
     seed = 7000 + H * 100 + D

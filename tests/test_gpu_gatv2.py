@@ -23,7 +23,9 @@ from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, samp
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(h, d) for h in (1, 2, 4, 8) for d in (32, 64, 128)]
+SHAPES = [(h, d) for h in (1, 2, 4, 8) for d in (32, 64, 128, 256)]
+BF16_ONLY = [(1, 512), (2, 512), (4, 512)]  # a 512-element fp32 head exceeds 64 lanes of 16 B
+CASES = [(h, d, t) for (h, d) in SHAPES for t in ("f32", "bf16")] + [(h, d, "bf16") for (h, d) in BF16_ONLY]
 FORCED_SPLIT = {"light_max_deg": 2, "heavy_min_deg": 6, "chunk_edges": 64, "grid_blocks": 0}
 SLOPE = 0.2
 
@@ -67,8 +69,7 @@ def check(rowptr, colidx, Lf, Rf, att, slope, dtype, tuning=None, rows=None):
 
 
 @pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("H,D", SHAPES)
+@pytest.mark.parametrize("H,D,dtype", CASES)
 def test_gatv2_ragged_small(H, D, dtype, split):
     N = 300
     seed = 7000 + H * 1000 + D
