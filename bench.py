@@ -20,7 +20,8 @@ microbenchmark under both mappings and load widths on original, random and
 reverse Cuthill-McKee node orders, plus the attention forward under each
 order) and prints one JSON line per measurement; ``--ablate-degree`` times the
 attention forward under the degree-aware partition and two degree-agnostic
-mappings (one lane group per row; one wavefront per row).
+mappings (one lane group per row; one wavefront per row); ``--hd-sweep``
+times the forward over the paper's (H, D) grid on one graph.
 """
 from __future__ import annotations
 
@@ -228,6 +229,44 @@ def run_ablation(args, gt, torch, to_device, synth) -> int:
     return 0
 
 
+PAPER_HD_GRID = [(2, 128), (2, 256), (4, 64), (4, 128), (8, 32), (8, 64)]
+
+
+def run_hd_sweep(args, gt, torch, to_device, synth) -> int:
+    """The paper's graph-transformer (H, D) grid on one graph: the attention
+    forward at each shape, with the graph's structure fixed and features
+    N(0, 1) of that shape; one JSON line per shape."""
+    import math
+    w = synth.config(args.config)
+    rp, ci = to_device(w.rowptr), to_device(w.colidx)
+    for H, D in PAPER_HD_GRID:
+        Q, K, V = synth.features(args.config, w.N, H, D, args.sweep_dtype)
+        q, k, v = (to_device(a) for a in (Q, K, V))
+        out = torch.empty_like(q)
+        scale = 1.0 / math.sqrt(D)
+        step = lambda: gt.gt_attn_fwd_ex(rp, ci, q, k, v, out, scale)
+        ms = _time_calls(torch, step, args.steps)
+        gt.gt_profile_enable(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        phase_ms, calls = gt.gt_profile_collect()
+        gt.gt_profile_enable(False)
+        kern_ms = phase_ms[1] / calls
+        eb = 4 if args.sweep_dtype == "f32" else 2
+        R = H * D * eb
+        mbytes = 8 * (w.N + 1) + 4 * w.E + w.N * R + 2 * w.E * R + w.N * R
+        print(json.dumps({"sweep": "paper (H, D) grid", "graph": w.name, "N": w.N, "E": w.E, "H": H,
+                          "D": D, "dtype": args.sweep_dtype, "ms_per_call": round(ms, 5),
+                          "GEdges_per_s": round(w.E / (ms * 1e-3) / 1e9, 4),
+                          "attention_kernel_ms": round(kern_ms, 5),
+                          "model_GBps": round(mbytes / (kern_ms * 1e-3) / 1e9, 1),
+                          "frac_of_8TBps": round(mbytes / (kern_ms * 1e-3) / 8e12, 4)}), flush=True)
+        del q, k, v, out
+        torch.cuda.empty_cache()
+    return 0
+
+
 def gatv2_attention_vector(w, seed: int):
     import math
     import synth
@@ -382,6 +421,10 @@ def main() -> int:
     ap.add_argument("--ablate-degree", action="store_true",
                     help="time degree-aware versus degree-agnostic work allocation")
     ap.add_argument("--ablate-configs", default="1,2,3,4", help="graphs of the ablation (indices)")
+    ap.add_argument("--hd-sweep", action="store_true",
+                    help="time the attention forward over the paper's (H, D) grid on --config's graph")
+    ap.add_argument("--sweep-dtype", choices=["f32", "bf16"], default="f32",
+                    help="feature dtype of --hd-sweep (default f32)")
     ap.add_argument("--study-features", default="32,128,512", help="feature widths of the study")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
                     help="enable the matrix-core path for dense 64-id windows holding at "
@@ -410,6 +453,8 @@ def main() -> int:
         return run_study(args, gt, torch, to_device, synth)
     if args.ablate_degree:
         return run_ablation(args, gt, torch, to_device, synth)
+    if args.hd_sweep:
+        return run_hd_sweep(args, gt, torch, to_device, synth)
     w = synth.config(args.config)
     if args.backward:
         print(json.dumps(run_backward(args, w, gt, torch, to_device, synth)), flush=True)
