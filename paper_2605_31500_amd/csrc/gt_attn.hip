@@ -1318,16 +1318,18 @@ struct Args {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Capacities of the partition's lists for E entries.  Split rows have degree
-// > chunk >= heavy_min, so they number at most E/heavy_min; front rows too.
-// A split row of degree d has fewer than 2d/chunk chunks, so work items are at
-// most E/heavy_min + 2E/chunk and partial-state slots at most 2E/chunk.
+// > chunk, so they number at most E/(chunk+1); front rows (degree >=
+// heavy_min) at most E/heavy_min.  A split row of degree d has fewer than
+// 2d/chunk chunks, so work items are at most E/heavy_min + 2E/chunk and
+// partial-state slots at most 2E/chunk.  The merge kernel's grid follows the
+// split-row bound.
 struct PartCaps {
     int64_t heavy, items, slots;
 };
 
 PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
     PartCaps c;
-    c.heavy = E / heavy_min + 1;
+    c.heavy = E / ((int64_t)chunk + 1) + 1;
     c.slots = 2 * (E / chunk) + 1;
     c.items = E / heavy_min + c.slots;
     return c;

@@ -102,6 +102,51 @@ def test_non_default_stream():
     assert np.array_equal(a, b)
 
 
+def test_concurrent_host_threads_and_streams():
+    """Four host threads, each with its own stream (and so its own cached
+    workspace), issue interleaved calls on different graphs and settings; every
+    result equals the same call made alone."""
+    import threading
+    import paper_2605_31500_amd as gtm
+    cases = []
+    for t in range(4):
+        N, H, D = 3000 + 500 * t, 4, 32
+        rowptr, colidx = synth.ragged_graph(40 + t, N, max_deg=30, hubs={5: N - 1, 9: 2000})
+        Q, K, V = synth.features(40 + t, N, H, D, "f32" if t % 2 == 0 else "bf16")
+        tuning = None if t < 2 else {"light_max_deg": 4, "heavy_min_deg": 32, "chunk_edges": 64,
+                                    "grid_blocks": 0}
+        want = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.2), tuning=tuning)
+        dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+        cases.append((dev, tuning, want))
+    torch.cuda.synchronize()
+    results, errors = [None] * 4, []
+
+    def work(t):
+        try:
+            dev, tuning, _ = cases[t]
+            s = torch.cuda.Stream()
+            outs = []
+            with torch.cuda.stream(s):
+                for _ in range(5):
+                    out = torch.empty_like(dev[2])
+                    gtm.gt_attn_fwd_ex(*dev, out, np.float32(0.2), tuning=tuning, stream=s)
+                    outs.append(out)
+            s.synchronize()
+            results[t] = [to_host_f32(o) for o in outs]
+        except Exception as e:  # reported below, in the test's own thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(4)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors
+    for t in range(4):
+        for got in results[t]:
+            assert np.array_equal(got, cases[t][2])
+
+
 def test_offsets_beyond_4_gib():
     """Feature tensors larger than 2^32 bytes, with every edge touching rows
     whose byte offset is past 4 GiB (64-bit address arithmetic)."""
