@@ -372,10 +372,55 @@ def cpu_baseline(w, seconds: float, att=None) -> dict:
         el = time.perf_counter() - t0
         if el >= seconds:
             break
-    return {"value": round(w.E * passes / el / 1e9, 6), "unit": "GEdges/s",
-            "cores": oracle.threads(), "kind": "oracle",
-            "sample": "all %d rows (%d CSR entries) of the same workload, %d pass(es), %.1f s"
-                      % (w.N, w.E, passes, el)}
+    return dict({"value": round(w.E * passes / el / 1e9, 6), "unit": "GEdges/s",
+                 "cores": oracle.threads(), "kind": "oracle",
+                 "sample": "all %d rows (%d CSR entries) of the same workload, %d pass(es), %.1f s"
+                           % (w.N, w.E, passes, el)}, **host_description())
+
+
+def host_description() -> dict:
+    """The CPUs this process may run on and their model name."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
+def call_stats(torch, fn, calls: int, flush=None) -> dict:
+    """Each call timed alone with HIP events on the current stream (mean, median,
+    min in ms).  With `flush`, it runs before each call, outside the timed
+    events (a cold L2 and Infinity Cache)."""
+    import numpy as np
+    fn()
+    times = []
+    for _ in range(calls):
+        if flush is not None:
+            flush()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    t = np.array(times)
+    return {"mean_ms": round(float(t.mean()), 5), "median_ms": round(float(np.median(t)), 5),
+            "min_ms": round(float(t.min()), 5), "calls": calls}
+
+
+def stored_l2_hit_rate(workload: str):
+    try:
+        entry = json.load(open(TRAFFIC_FILE)).get(workload)
+    except (OSError, ValueError):
+        return None
+    if not entry or entry.get("kernel_source_sha256_16") != source_hash():
+        return None
+    return entry.get("l2_hit_rate")
 
 
 def copy_calibration(mib: int, steps: int) -> int:
@@ -537,7 +582,18 @@ def main() -> int:
                       "merge": round(phase_ms[2] / calls, 5)},
         "whole_call_model_GBps": round(mbytes / (ms_per_step * 1e-3) / 1e9, 1),
         "compulsory_bytes": compulsory_bytes(w, args.gatv2),
+        "edge_heads_per_s": round(w.E * w.H / (ms_per_step * 1e-3), 1),
     }
+    key = w.name + (":gatv2" if args.gatv2 else "")
+    rec["roofline"]["l2_hit_rate"] = stored_l2_hit_rate(key)
+    if traffic:
+        rec["roofline"]["traffic_over_model"] = round(traffic / mbytes, 4)
+    # per-call statistics, warm and with L2 and the Infinity Cache evicted by a
+    # 1 GiB write before each call (outside the timed events)
+    rec["call_stats"] = call_stats(torch, step, 30)
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device=dev[2].device)
+    rec["cold_call_stats"] = call_stats(torch, step, 10, flush=lambda: scratch.fill_(1.0))
+    del scratch
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, att)
     print(json.dumps(rec), flush=True)
