@@ -716,20 +716,21 @@ struct TileLds {
     static constexpr int HD = H * D;
     static constexpr int KST = HD + 8;  // padded K row (bf16 elements)
     int64_t rp[kWin + 1];
-    int32_t lpre[kWin + 1];              // prefix of light-row degrees
-    int32_t ebeg[kWin], eend[kWin];      // each row's entries within idx
-    int32_t idx[kWin * kWinMaxDeg];      // the window's entries (see staging)
     uint64_t masks[kWin];
     int32_t wave_cnt[kWavesPerBlock];
+    // The K and V tiles are dead once the products are done; the strip results
+    // and the index tiles of the remaining-entry stream then reuse their space.
     union alignas(16) {
         struct {
             uint16_t k[kWin][KST];
             uint16_t vt[HD][kVtStride];
         } kv;
-        float acc[kWavesPerBlock][16][HD + 4];  // padded: the MFMA-layout writes hit distinct banks
+        struct {
+            float acc[kWavesPerBlock][16][HD + 4];  // padded: the MFMA-layout writes hit distinct banks
+            int32_t ctile[kWavesPerBlock][kWave / (H * D / 8) * kWinMaxDeg];  // per lane group: one row's entries
+        } rest;
     } big;
     float2 ml[kWavesPerBlock][16][H];
-    int32_t ctile[kWavesPerBlock][kWave / (H * D / 8) * kWinMaxDeg];  // per lane group: one row's entries
 };
 
 template <int H, int D>
@@ -745,6 +746,17 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
     const int g16 = lane >> 4, n16 = lane & 15;  // MFMA lane coordinates
     const int64_t r0 = (int64_t)blockIdx.x * kWin;
     const int64_t wend = r0 + kWin;
+
+    // bounds of this lane's row in the mask stage (4 lanes per row), loaded
+    // first so that its entries can be requested right after the staging loads
+    const int srow = lane >> 2, sub = lane & 3;
+    const int wrow = 16 * wv + srow;  // row within the window
+    const int64_t r = r0 + wrow;
+    int64_t mb = 0, me = 0;
+    if (r < p.N) {
+        mb = p.rowptr[r];
+        me = p.rowptr[r + 1];
+    }
 
     // ---- 1. staging
     if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
@@ -779,67 +791,31 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
         qreg[t] = make_uint4(0, 0, 0, 0);
         if (qrow < p.N) qreg[t] = *reinterpret_cast<const uint4*>(p.Q + (qrow * HD + 32 * t + 8 * g16) * 2);
     }
-    __syncthreads();
-    // Entries: if the window's whole CSR range fits, it is copied as is (one
-    // coalesced pass); otherwise only the light rows' entries are packed.
-    const int64_t n_all = lds.rp[kWin] - lds.rp[0];
-    const bool contiguous = n_all <= kWin * kWinMaxDeg;
-    if (wv == 0) {
-        const int64_t deg = lds.rp[lane + 1] - lds.rp[lane];
-        int x = (deg <= p.light_max) ? (int)deg : 0;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-            const int y = __shfl_up(x, o);
-            if (lane >= o) x += y;
-        }
-        lds.lpre[lane + 1] = x;
-        if (lane == 0) lds.lpre[0] = 0;
-        if (contiguous) {
-            lds.ebeg[lane] = (int32_t)(lds.rp[lane] - lds.rp[0]);
-            lds.eend[lane] = (int32_t)(lds.rp[lane + 1] - lds.rp[0]);
-        } else {
-            lds.eend[lane] = x;
-            lds.ebeg[lane] = (deg <= p.light_max) ? x - (int)deg : x;
-        }
-    }
-    __syncthreads();
-    {
-        constexpr int kPer = kWin * kWinMaxDeg / kBlock;  // entries per thread
-        const int n_ent = contiguous ? (int)n_all : lds.lpre[kWin];
-        int32_t vals[kPer];
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int f = tid + k * kBlock;
-            int64_t src = lds.rp[0] + f;
-            if (!contiguous && f < n_ent) {
-                int lo = 0, hi = kWin;  // owner row: the last row with lpre[row] <= f
-                while (hi - lo > 1) {
-                    const int mid = (lo + hi) >> 1;
-                    if (lds.lpre[mid] <= f) lo = mid; else hi = mid;
-                }
-                src = lds.rp[lo] + (f - lds.lpre[lo]);
-            }
-            vals[k] = f < n_ent ? p.colidx[src] : 0;
-        }
-#pragma unroll
-        for (int k = 0; k < kPer; ++k)
-            if (tid + k * kBlock < n_ent) lds.idx[tid + k * kBlock] = vals[k];
-    }
-    __syncthreads();
 
-    // ---- 2. in-window masks: 4 lanes per row, 16 rows per wave
-    const int srow = lane >> 2, sub = lane & 3;
-    const int wrow = 16 * wv + srow;  // row within the window
-    const int64_t r = r0 + wrow;
-    const bool light = r < p.N && (lds.rp[wrow + 1] - lds.rp[wrow]) <= p.light_max;
-    const int lb = lds.ebeg[wrow], le = light ? lds.eend[wrow] : lds.ebeg[wrow];
+    // ---- 2. in-window masks: 4 lanes per row, 16 rows per wave.  The entries
+    // come straight from colidx (one batch of independent loads, overlapping
+    // the staging above); the remaining-entry stream reads them again later,
+    // so the window needs no LDS copy of its entries.
+    const bool light = r < p.N && (me - mb) <= p.light_max;
+    constexpr int kMaskPer = kWinMaxDeg / 4;  // entries per lane (light_max <= kWinMaxDeg)
+    int32_t ent[kMaskPer] = {};
+    if (light && me > mb) {
+#pragma unroll
+        for (int k = 0; k < kMaskPer; ++k) {
+            const int64_t pos = mb + sub + 4 * k;
+            ent[k] = p.colidx[pos < me ? pos : me - 1];
+        }
+    }
     uint64_t mk = 0;
     int cnt = 0;
-    for (int t = lb + sub; t < le; t += 4) {
-        const int64_t j = lds.idx[t];
-        if (j >= r0 && j < wend) {
-            mk |= 1ull << (j - r0);
-            ++cnt;
+    if (light) {
+#pragma unroll
+        for (int k = 0; k < kMaskPer; ++k) {
+            const int64_t j = ent[k];
+            if (mb + sub + 4 * k < me && j >= r0 && j < wend) {
+                mk |= 1ull << (j - r0);
+                ++cnt;
+            }
         }
     }
     mk |= shfl_xor_u64(mk, 1);
@@ -936,7 +912,7 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
 #pragma unroll
             for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) lds.big.acc[wv][4 * g16 + i][h * D + 16 * dt + n16] = oacc[h][dt][i];
+                for (int i = 0; i < 4; ++i) lds.big.rest.acc[wv][4 * g16 + i][h * D + 16 * dt + n16] = oacc[h][dt][i];
             if (g16 == 0) lds.ml[wv][n16][h] = make_float2(mx[h], lsum[h]);
         }
     }
@@ -944,7 +920,7 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
 
     // ---- 4. remaining entries of each light row, CSR online softmax, output
     const int g = lane / G, lig = lane % G;
-    int32_t* gtile = lds.ctile[wv] + g * kWinMaxDeg;
+    int32_t* gtile = lds.big.rest.ctile[wv] + g * kWinMaxDeg;
     for (int pass = 0; pass < 16 / P; ++pass) {
         const int sr = pass * P + g;
         if (!((light_bits >> (4 * sr)) & 1ull)) continue;
@@ -961,15 +937,25 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
                 st.m[k] = ml.x;
                 st.l[k] = ml.y;
 #pragma unroll
-                for (int q = 0; q < Gm::kEPV; ++q) st.acc[k][q] = lds.big.acc[wv][sr][v * Gm::kEPV + q];
+                for (int q = 0; q < Gm::kEPV; ++q) st.acc[k][q] = lds.big.rest.acc[wv][sr][v * Gm::kEPV + q];
             }
         }
         // gather the row's remaining entries (outside the tile) into gtile
-        const int eb = lds.ebeg[wr], ee = lds.eend[wr];
+        const int64_t eb = lds.rp[wr], ee = lds.rp[wr + 1];  // a light row: at most kWinMaxDeg entries
+        constexpr int kRowPer = (kWinMaxDeg + G - 1) / G;
+        int32_t re[kRowPer] = {};
+        if (ee > eb) {
+#pragma unroll
+            for (int k = 0; k < kRowPer; ++k) {
+                const int64_t pos = eb + lig + k * G;
+                re[k] = p.colidx[pos < ee ? pos : ee - 1];
+            }
+        }
         int n_take = 0;
-        for (int tb = eb; tb < ee; tb += G) {
-            const bool in = tb + lig < ee;
-            const int32_t idx = lds.idx[in ? tb + lig : ee - 1];
+#pragma unroll
+        for (int k = 0; k < kRowPer; ++k) {
+            const bool in = eb + lig + k * G < ee;
+            const int32_t idx = re[k];
             const bool take = in && !(use_tile && idx >= r0 && idx < wend);
             const uint64_t bal = __ballot(take);
             const uint32_t gbits = (uint32_t)((bal >> (g * G)) & ((1ull << G) - 1));

@@ -106,3 +106,23 @@ def test_tiles_full_sbm_sampled():
     w = synth.config(3)
     rows = sample_rows(w.rowptr, n_random=3000, n_top=64)
     check(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, tiles=256, rows=rows)
+
+
+def test_tiles_rows_at_the_degree_limit():
+    # light rows in tile mode hold at most 64 entries: a row of all 64 window
+    # ids (full mask), one of 64 out-of-window entries (all streamed), a 32/32
+    # mix, 63 entries, and a 65-entry row that belongs to the CSR kernel
+    N = 64 * 6 + 11
+    rp, ci = synth.sbm_graph(24, N, 64, 4)
+    rows = [list(ci[rp[i]:rp[i + 1]]) for i in range(N)]
+    outside = [j for j in range(N) if j // 64 != 1]
+    rows[10] = list(range(64))
+    rows[75] = outside[5:69]
+    rows[140] = list(range(128, 160)) + outside[100:132]
+    rows[141] = list(range(128, 192)) + [3]
+    rows[142] = list(range(128, 191))
+    rowptr, colidx = csr_from_rows(rows)
+    assert [int(rowptr[i + 1] - rowptr[i]) for i in (10, 75, 140, 141, 142)] == [64, 64, 64, 65, 63]
+    Q, K, V = synth.features(24, N, 2, 64, "bf16")
+    for tiles in (1, 256):
+        check(rowptr, colidx, Q, K, V, np.float32(0.125), tiles=tiles)
