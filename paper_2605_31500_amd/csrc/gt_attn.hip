@@ -733,8 +733,16 @@ struct TileLds {
     float2 ml[kWavesPerBlock][16][H];
 };
 
+// Four workgroups per CU fit the LDS of a window (about 40 KB) when H*D <= 128
+// and H <= 2; those shapes are held to 128 VGPRs so that registers allow it too.
 template <int H, int D>
-__global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
+struct TileWaves {
+    static constexpr int value = H <= 2 ? 4 : 1;
+};
+
+template <int H, int D>
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(TileWaves<H, D>::value)))
+gt_tile_kernel(TileParams p) {
     using Gm = Geo<bf16_tag, H, D>;
     using L = TileLds<H, D>;
     constexpr int HD = H * D;
@@ -918,10 +926,31 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
     }
     wave_lds_fence();
 
-    // ---- 4. remaining entries of each light row, CSR online softmax, output
+    // ---- 4. remaining entries of each light row, CSR online softmax, output.
+    // Each lane group takes rows g, g + P, ... of the wave's strip; the entries
+    // of a group's next row are requested before the current row's gathers.
     const int g = lane / G, lig = lane % G;
     int32_t* gtile = lds.big.rest.ctile[wv] + g * kWinMaxDeg;
-    for (int pass = 0; pass < 16 / P; ++pass) {
+    constexpr int kRowPer = (kWinMaxDeg + G - 1) / G;  // a light row: at most kWinMaxDeg entries
+    constexpr int kPasses = 16 / P;
+    auto load_entries = [&](int pass, int32_t (&e)[kRowPer]) {
+        const int sr = pass * P + g, wr = 16 * wv + sr;
+        const int64_t eb = lds.rp[wr], ee = lds.rp[wr + 1];
+        if (((light_bits >> (4 * sr)) & 1ull) && ee > eb) {
+#pragma unroll
+            for (int k = 0; k < kRowPer; ++k) {
+                const int64_t pos = eb + lig + k * G;
+                e[k] = p.colidx[pos < ee ? pos : ee - 1];
+            }
+        }
+    };
+    int32_t nxt[kRowPer] = {};
+    load_entries(0, nxt);
+    for (int pass = 0; pass < kPasses; ++pass) {
+        int32_t re[kRowPer];
+#pragma unroll
+        for (int k = 0; k < kRowPer; ++k) re[k] = nxt[k];
+        if (pass + 1 < kPasses) load_entries(pass + 1, nxt);
         const int sr = pass * P + g;
         if (!((light_bits >> (4 * sr)) & 1ull)) continue;
         const bool use_tile = dense && ((ok_bits >> (4 * sr)) & 1ull);
@@ -940,17 +969,8 @@ __global__ void __launch_bounds__(kBlock) gt_tile_kernel(TileParams p) {
                 for (int q = 0; q < Gm::kEPV; ++q) st.acc[k][q] = lds.big.rest.acc[wv][sr][v * Gm::kEPV + q];
             }
         }
-        // gather the row's remaining entries (outside the tile) into gtile
-        const int64_t eb = lds.rp[wr], ee = lds.rp[wr + 1];  // a light row: at most kWinMaxDeg entries
-        constexpr int kRowPer = (kWinMaxDeg + G - 1) / G;
-        int32_t re[kRowPer] = {};
-        if (ee > eb) {
-#pragma unroll
-            for (int k = 0; k < kRowPer; ++k) {
-                const int64_t pos = eb + lig + k * G;
-                re[k] = p.colidx[pos < ee ? pos : ee - 1];
-            }
-        }
+        // the row's remaining entries (outside the tile) into gtile
+        const int64_t eb = lds.rp[wr], ee = lds.rp[wr + 1];
         int n_take = 0;
 #pragma unroll
         for (int k = 0; k < kRowPer; ++k) {
