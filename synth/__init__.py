@@ -175,7 +175,12 @@ def rmat_graph(seed: int, scale: int, a: float, b: float, c: float, avg_deg: int
 
 def sbm_graph(seed: int, N: int, block: int, n_out: int):
     """Contiguous blocks of `block` ids; intra-block pairs w.p. 1/2; n_out
-    distinct uniform sources outside the block; self-loop."""
+    distinct uniform sources outside the block; self-loop.  Every block must
+    leave at least n_out ids outside it (the draw of distinct sources would
+    not end otherwise)."""
+    if block < 1 or n_out < 0 or (n_out > 0 and N - min(block, N) < n_out):
+        raise ValueError("sbm_graph: %d ids outside a block of %d cannot give %d distinct sources"
+                         % (N - min(block, N), block, n_out))
     rowptr = np.empty(N + 1, dtype=np.int64)
     lib().synth_sbm(seed, STREAM_GRAPH, N, block, n_out, _p(rowptr), None)
     colidx = np.empty(int(rowptr[-1]), dtype=np.int32)

@@ -126,3 +126,12 @@ def test_tiles_rows_at_the_degree_limit():
     Q, K, V = synth.features(24, N, 2, 64, "bf16")
     for tiles in (1, 256):
         check(rowptr, colidx, Q, K, V, np.float32(0.125), tiles=tiles)
+
+
+@pytest.mark.parametrize("N", [1, 5, 63, 64, 65, 129])
+def test_tiles_graphs_smaller_than_or_near_a_window(N):
+    # one partial window, exactly one, and one full window plus a few rows
+    rp, ci = synth.sbm_graph(25 + N, N, 64, 4 if N >= 68 else 0)
+    Q, K, V = synth.features(25 + N, N, 2, 64, "bf16")
+    for tiles in (1, 256):
+        check(rp, ci, Q, K, V, np.float32(0.125), tiles=tiles)

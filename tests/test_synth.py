@@ -86,6 +86,17 @@ def test_sbm_recipe_small():
     assert np.sum(rows == ci) == N
 
 
+def test_sbm_partial_block_and_impossible_out_degree():
+    # a partial last block still gets its out-of-block sources
+    rp, ci = synth.sbm_graph(3, 64 + 10, 64, 4)
+    synth.check_csr(rp, ci, 74)
+    rows = np.repeat(np.arange(74), np.diff(rp))
+    assert np.all(np.bincount(rows[(rows // 64) != (ci // 64)], minlength=74) == 4)
+    # fewer ids outside a block than distinct sources asked for is refused
+    with pytest.raises(ValueError):
+        synth.sbm_graph(3, 65, 64, 4)
+
+
 def test_lognormal_recipe_small():
     N = 100_000
     rp, ci = synth.lognormal_graph(0, N, total=3_000_000)
