@@ -154,3 +154,32 @@ def test_dot_aggr_host_validation(lib, kw, status):
     assert lib.gt_dot_aggr(P(a["rowptr"]), P(a["colidx"]), P(a["X"]), P(a["out"]), a["N"], a["E"],
                            a["F"], a["mapping"], a["load_bytes"], None) == status
     assert lib.gt_last_error_message()
+
+
+def call_bwd(lib, dtype=0, rowptr=FAKE, colidx=FAKE, rowptr_t=FAKE, colidx_t=FAKE, Q=FAKE,
+             K=FAKE + 0x100000, V=FAKE + 0x200000, out=FAKE + 0x300000, dout=FAKE + 0x400000,
+             lse=FAKE + 0x500000, dQ=FAKE + 0x600000, dK=FAKE + 0x700000, dV=FAKE + 0x800000,
+             N=10, E=20, H=4, D=32, scale=0.1):
+    P = ctypes.c_void_p
+    return lib.gt_attn_bwd(dtype, P(rowptr), P(colidx), P(rowptr_t), P(colidx_t), P(Q), P(K), P(V),
+                           P(out), P(dout), P(lse), P(dQ), P(dK), P(dV), N, E, H, D,
+                           ctypes.c_float(scale), None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=5), 2), (dict(H=3), 2), (dict(D=48), 2), (dict(dtype=1, H=8, D=512), 2),
+    (dict(N=-1), 1), (dict(E=-1), 1), (dict(H=0), 1), (dict(scale=float("inf")), 1),
+    (dict(rowptr_t=0), 1), (dict(colidx_t=0), 1), (dict(dout=0), 1),
+    (dict(lse=0), 1), (dict(lse=FAKE + 0x500002), 1),          # lse null / misaligned
+    (dict(dQ=0), 1), (dict(dK=FAKE + 0x700004), 1),            # gradient null / misaligned
+    (dict(dQ=FAKE), 1),                                        # dQ aliases Q
+    (dict(dV=FAKE + 0x700000 + 1024), 1),                      # dV overlaps dK
+    (dict(dK=FAKE + 0x500000), 1),                             # dK overlaps lse
+])
+def test_bwd_host_validation(lib, kw, status):
+    assert call_bwd(lib, **kw) == status
+    assert lib.gt_last_error_message()
+
+
+def test_bwd_empty_graph_is_a_no_op(lib):
+    assert call_bwd(lib, N=0, E=0) == 0
