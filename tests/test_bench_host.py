@@ -76,3 +76,9 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_paper_context_is_labelled():
+    # the paper's ratios are quoted with their hardware and quantity, never as a target
+    for key, ctx in bench.PAPER_CONTEXT.items():
+        assert "A100" in ctx["hardware"] and "t_DGL / t" in ctx["quantity"], key
