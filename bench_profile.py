@@ -61,7 +61,8 @@ CAPTURES = {
 }
 SQ_GROUP = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_INSTS_LDS", "SQ_INSTS_VALU", "SQ_INSTS_VMEM_RD",
             "SQ_WAVES", "GRBM_GUI_ACTIVE"]
-COUNTER_GROUPS = [["FETCH_SIZE"], ["WRITE_SIZE"], ["TCC_HIT_sum", "TCC_MISS_sum"], SQ_GROUP]
+TA_GROUP = ["TA_TA_BUSY_sum", "TA_ADDR_STALLED_BY_TC_CYCLES_sum", "GRBM_GUI_ACTIVE"]
+COUNTER_GROUPS = [["FETCH_SIZE"], ["WRITE_SIZE"], ["TCC_HIT_sum", "TCC_MISS_sum"], SQ_GROUP, TA_GROUP]
 COPY_MIB = 1024
 N_XCD, N_CU = 8, 256
 
@@ -214,6 +215,7 @@ def summarize(out, mode, source_hash):
     write, _ = counters(d, ["WRITE_SIZE"], kernels)
     l2, _ = counters(d, ["TCC_HIT_sum", "TCC_MISS_sum"], kernels)
     sq, _ = counters(d, SQ_GROUP, kernels)
+    ta, _ = counters(d, TA_GROUP, kernels)
     fb = fetch["FETCH_SIZE"] * 1024 * fscale
     wb = write["WRITE_SIZE"] * 1024 * wscale
     alg = live["roofline"]["algorithmic_bytes_per_launch"]
@@ -221,6 +223,8 @@ def summarize(out, mode, source_hash):
     cycles = sq["GRBM_GUI_ACTIVE"] / N_XCD
     valu = sq["SQ_INSTS_VALU"] / (N_CU * cycles)
     conf = sq["SQ_LDS_BANK_CONFLICT"] / max(sq["SQ_LDS_IDX_ACTIVE"] - sq["SQ_LDS_BANK_CONFLICT"], 1.0)
+    ta_cycles = ta["GRBM_GUI_ACTIVE"] / N_XCD
+    ta_busy = ta["TA_TA_BUSY_sum"] / (N_CU * ta_cycles)  # one texture-address unit per CU
     kl = " + ".join("`%s`" % k[0] for k in main)
     L = ["# %s on %s" % (spec["title"], w), "",
          "Library sources (`paper_2605_31500_amd/csrc/*.hip`, `*.hpp`), sha256[:16] as computed by "
@@ -250,7 +254,11 @@ def summarize(out, mode, source_hash):
           "| VALU issue share | SQ_INSTS_VALU %.3g / (%d CUs × GRBM_GUI_ACTIVE %.3g / %d XCDs) | %.1f %% |"
           % (sq["SQ_INSTS_VALU"], N_CU, sq["GRBM_GUI_ACTIVE"], N_XCD, 100 * valu),
           "| LDS instructions, vector-memory reads, waves | SQ_INSTS_LDS, SQ_INSTS_VMEM_RD, SQ_WAVES | "
-          "%.3g, %.3g, %.0f |" % (sq["SQ_INSTS_LDS"], sq["SQ_INSTS_VMEM_RD"], sq["SQ_WAVES"]), "",
+          "%.3g, %.3g, %.0f |" % (sq["SQ_INSTS_LDS"], sq["SQ_INSTS_VMEM_RD"], sq["SQ_WAVES"]),
+          "| texture-address unit busy | TA_TA_BUSY_sum %.3g / (%d CUs × GRBM_GUI_ACTIVE %.3g / %d XCDs) | %.1f %% |"
+          % (ta["TA_TA_BUSY_sum"], N_CU, ta["GRBM_GUI_ACTIVE"], N_XCD, 100 * ta_busy),
+          "| texture-address stalls on the cache | TA_ADDR_STALLED_BY_TC_CYCLES_sum / TA_TA_BUSY_sum | %.3f |"
+          % (ta["TA_ADDR_STALLED_BY_TC_CYCLES_sum"] / max(ta["TA_TA_BUSY_sum"], 1.0)), "",
           "Algorithmic bytes per call (%s): %.4f GB; measured HBM / algorithmic = %.3f. FETCH_SIZE counts L2 "
           "misses sent to the fabric, which the 256 MB Infinity Cache may serve, so it bounds DRAM reads from "
           "above. The VALU share counts one wave-level VALU instruction per CU per cycle as the issue limit "
@@ -274,8 +282,8 @@ def summarize(out, mode, source_hash):
         tj[spec["key"].format(w=w, g=g)] = entry
         with open(tf, "w") as f:
             json.dump(tj, f, indent=1, sort_keys=True)
-    print("%-55s kernel %9.2f us  HBM %.3f GB  HBM/model %.3f  L2 hit %.3f  VALU %.2f  LDS conflicts %.3f"
-          % (name, kavg, (fb + wb) / 1e9, (fb + wb) / alg, hit, valu, conf), flush=True)
+    print("%-55s kernel %9.2f us  HBM %.3f GB  HBM/model %.3f  L2 hit %.3f  VALU %.2f  TA %.2f  LDS conflicts %.3f"
+          % (name, kavg, (fb + wb) / 1e9, (fb + wb) / alg, hit, valu, ta_busy, conf), flush=True)
     return name, entry
 
 

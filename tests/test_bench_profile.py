@@ -46,6 +46,8 @@ def capture(tmp_path, monkeypatch):
               "TCC_HIT_sum_TCC_MISS_sum": {"TCC_HIT_sum": 25.0, "TCC_MISS_sum": 75.0},
               "_".join(bp.SQ_GROUP): {"SQ_LDS_BANK_CONFLICT": 0.0, "SQ_LDS_IDX_ACTIVE": 10.0, "SQ_INSTS_LDS": 1.0,
                                       "SQ_INSTS_VALU": 256.0 * 100, "SQ_INSTS_VMEM_RD": 5.0, "SQ_WAVES": 64.0,
+                                      "GRBM_GUI_ACTIVE": 8 * 200.0},
+              "_".join(bp.TA_GROUP): {"TA_TA_BUSY_sum": 256.0 * 150, "TA_ADDR_STALLED_BY_TC_CYCLES_sum": 100.0,
                                       "GRBM_GUI_ACTIVE": 8 * 200.0}}
     for g, vals in groups.items():
         write_csv(str(d / ("pmc_" + g) / "x_counter_collection.csv"), hdr,
@@ -70,6 +72,7 @@ def test_summary_arithmetic(capture):
     text = (prof / (name + ".md")).read_text()
     assert "| `gt_attn_kernel<float, 4, 32, 0>` | 10 | 200.00 |" in text
     assert "VALU issue share" in text and "| 50.0 % |" in text  # 25600 / (256 x 1600/8)
+    assert "texture-address unit busy" in text and "| 75.0 % |" in text  # 38400 / (256 x 200)
     assert "-- python3 %s --steps 50" % bp.BENCH in text     # the program follows `--` directly
     assert "rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum" in text
 
