@@ -339,7 +339,7 @@ def run_backward(args, w, gt, torch, to_device, synth) -> dict:
     ms = ev0.elapsed_time(ev1) / args.steps
     mbytes = backward_model_bytes(w)
     achieved = mbytes / (ms * 1e-3) / 1e9
-    return {
+    rec = {
         "metric": "fused graph-attention bwd GEdges/s at 1 MI355X; achieved HBM GB/s vs peak",
         "value": round(w.E / (ms * 1e-3) / 1e9, 4), "unit": "GEdges/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
@@ -352,6 +352,23 @@ def run_backward(args, w, gt, torch, to_device, synth) -> dict:
                      "traffic": stored_traffic(w.name + ":backward"),
                      "algorithmic_bytes_per_launch": mbytes, "kernel_ms": round(ms, 5)},
     }
+    if not args.no_cpu_baseline:
+        # the oracle's two gradient definitions (dQ by rows, dK and dV by columns)
+        import oracle
+        passes, t0 = 0, time.perf_counter()
+        while True:
+            oracle.gt_attn_bwd_dq(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale)
+            oracle.gt_attn_bwd_dkv(w.rowptr, w.colidx, rpt, cit, w.Q, w.K, w.V, dO, w.scale)
+            passes += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds:
+                break
+        rec["cpu_baseline"] = dict({"value": round(w.E * passes / el / 1e9, 6), "unit": "GEdges/s",
+                                    "cores": oracle.threads(), "kind": "oracle",
+                                    "sample": "all %d rows and %d columns (%d CSR entries) of the same workload, "
+                                              "%d pass(es), %.1f s" % (w.N, w.N, w.E, passes, el)},
+                                   **host_description())
+    return rec
 
 
 def source_hash() -> str:
