@@ -131,6 +131,7 @@ struct AttnParams {
     float* part_acc;   // [slot][H*D]
     float2* part_ml;   // [slot][H]: (running max in log2 units, sum)
     int32_t skip_light;  // light rows are handled by the dense-tile kernel
+    const int32_t* light_list;  // [N]: light rows in step order per partition block, -1 elsewhere
 };
 
 struct PartParams {
@@ -146,6 +147,8 @@ struct PartParams {
     int32_t* med_list;
     HeavyRow* heavy;
     ChunkItem* chunks;
+    int32_t* light_list = nullptr;  // or the block-local order of the light rows
+    int32_t step = 1;               // entries per step of the light-row loop (its step classes)
 };
 
 struct MergeParams {
@@ -550,6 +553,14 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
 // loaded while the current row's first K/V batch is in flight, so a short row
 // costs about one memory latency instead of three (rowptr -> colidx -> K/V).
 // An index tile holds LightTile<G>::kR * G entries (kR loads per lane).
+// Light rows in the partition's step order pay where a wave holds four or more
+// rows (its groups then wait on their longest row); with one or two rows per
+// wave the extra index load costs more than the balance gains.
+template <typename T, int H, int D>
+struct SortedLight {
+    static constexpr bool value = Geo<T, H, D>::kP >= 4;
+};
+
 template <int G> struct LightTile {
     static constexpr int kR = G >= 64 ? 1 : 2;
     static constexpr int kEntries = kR * G;
@@ -570,8 +581,19 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
             v[r] = p.colidx[pos < ce ? pos : ce - 1];
         }
     };
-    int64_t row = it * P + g;
-    bool ok = it < it_end && row < p.N;
+    // Item `it` is the group's row at position it * P + g of the light-row
+    // order (-1: none); the entry two items ahead is requested one item early,
+    // so that it is in a register when its row pointers are needed.
+    auto row_at = [&](int64_t i) -> int64_t {
+        const int64_t pos = i * P + g;
+        if constexpr (SortedLight<T, H, D>::value)
+            return (i < it_end && pos < p.N) ? (int64_t)p.light_list[pos] : -1;
+        else
+            return (i < it_end && pos < p.N) ? pos : -1;
+    };
+    int64_t row = row_at(it);
+    int64_t row_next = row_at(it + stride);
+    bool ok = row >= 0;
     int64_t b = ok ? p.rowptr[row] : 0, e = ok ? p.rowptr[row + 1] : 0;
     bool mine = ok && (e - b) <= p.light_max;
     int32_t idx[R] = {};
@@ -583,8 +605,9 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
 #pragma unroll
         for (int r = 0; r < R; ++r) tv[r] = idx[r];
         it += stride;
-        row = it * P + g;
-        ok = it < it_end && row < p.N;
+        row = row_next;
+        row_next = row_at(it + stride);
+        ok = row >= 0;
         b = ok ? p.rowptr[row] : 0;
         e = ok ? p.rowptr[row + 1] : 0;
         mine = ok && (e - b) <= p.light_max;
@@ -1003,6 +1026,7 @@ gt_tile_kernel(TileParams p) {
 // at least `chunk` entries each, so the ordered merge of a hub stays a few
 // load rounds long.
 constexpr int kMaxChunks = 32;
+constexpr int kLightClasses = 16;  // step-count classes of the light-row order
 
 __device__ __forceinline__ int block_exclusive_scan(int v, int* lds_waves, int* total) {
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
@@ -1036,12 +1060,14 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     __shared__ int wave_cnt[kPartRowsPerThread][kWavesPerBlock];
     __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock], scan_s[kWavesPerBlock];
     __shared__ int base[4];
+    __shared__ int cls_cnt[kLightClasses], cls_pos[kLightClasses];
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const int64_t r0 = (int64_t)blockIdx.x * kPartRowsPerBlock;
     int64_t rb[kPartRowsPerThread], deg[kPartRowsPerThread];
     bool med[kPartRowsPerThread];
     uint64_t mask[kPartRowsPerThread];
     int n_heavy = 0, n_chunk = 0, n_slot = 0;
+    if (p.light_list && threadIdx.x < kLightClasses) cls_cnt[threadIdx.x] = 0;
 #pragma unroll
     for (int k = 0; k < kPartRowsPerThread; ++k) {
         const int64_t r = r0 + k * kBlock + threadIdx.x;
@@ -1060,6 +1086,45 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
             n_chunk += nch;
             n_slot += nch > 1 ? nch : 0;
         }
+    }
+    if (p.light_list) {
+        // Light rows of this block in descending step count (a counting sort in
+        // LDS), so the lane groups of a wave take rows of similar length and a
+        // wave does not wait on one long row among short ones.  The order within
+        // a step class is arbitrary; every row is computed on its own, so the
+        // results do not depend on it.  Positions after the block's light rows
+        // hold -1.
+        __syncthreads();  // cls_cnt zeroed
+        int cls[kPartRowsPerThread];
+#pragma unroll
+        for (int k = 0; k < kPartRowsPerThread; ++k) {
+            const int64_t r = r0 + k * kBlock + threadIdx.x;
+            cls[k] = -1;
+            if (r < p.N && deg[k] <= p.light_max) {
+                const int64_t st = (deg[k] + p.step - 1) / p.step;
+                cls[k] = (int)(st < kLightClasses - 1 ? st : kLightClasses - 1);
+                atomicAdd(&cls_cnt[cls[k]], 1);
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int acc = 0;
+            for (int c = kLightClasses - 1; c >= 0; --c) {
+                cls_pos[c] = acc;
+                acc += cls_cnt[c];
+            }
+            cls_cnt[0] = acc;  // the block's light-row count (class 0's count is no longer needed)
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kPartRowsPerThread; ++k)
+            if (cls[k] >= 0) {
+                const int at = atomicAdd(&cls_pos[cls[k]], 1);
+                p.light_list[r0 + at] = (int32_t)(r0 + k * kBlock + threadIdx.x);
+            }
+        const int n_light_rows = cls_cnt[0];
+        const int64_t rows_here = (p.N - r0 < kPartRowsPerBlock) ? p.N - r0 : kPartRowsPerBlock;
+        for (int64_t j = n_light_rows + threadIdx.x; j < rows_here; j += kBlock) p.light_list[r0 + j] = -1;
     }
     int tot_h, tot_c, tot_s;
     const int off_h = block_exclusive_scan(n_heavy, scan_h, &tot_h);
@@ -1422,6 +1487,8 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const size_t o_chunks = off;   off = align_up(off + (size_t)caps.items * sizeof(ChunkItem), 256);
     const size_t o_ml = off;       off = align_up(off + (size_t)caps.slots * H * sizeof(float2), 256);
     const size_t o_acc = off;      off = align_up(off + (size_t)caps.slots * H * D * sizeof(float), 256);
+    const size_t o_light = off;
+    off = align_up(off + ((tiles || !SortedLight<T, H, D>::value) ? 0 : (size_t)a.N * sizeof(int32_t)), 256);
     const size_t ws_bytes = off;
 
     WsEntry& we = ws_entry(dev, stream);
@@ -1468,6 +1535,8 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
+    pp.light_list = (tiles || !SortedLight<T, H, D>::value) ? nullptr : reinterpret_cast<int32_t*>(ws + o_light);
+    pp.step = Gm::kU;
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
     ph.mark(1, stream);  // the attention phase includes the tile kernel
     if constexpr (kTileShape) {
@@ -1511,6 +1580,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
     ap.part_ml = reinterpret_cast<float2*>(ws + o_ml);
     ap.skip_light = tiles ? 1 : 0;
+    ap.light_list = pp.light_list;
     hipLaunchKernelGGL((gt_attn_kernel<T, H, D, KIND>), dim3(grid), dim3(kBlock), 0, stream, ap);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "attention launch");
     ph.mark(2, stream);
