@@ -554,11 +554,13 @@ __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, i
 // costs about one memory latency instead of three (rowptr -> colidx -> K/V).
 // An index tile holds LightTile<G>::kR * G entries (kR loads per lane).
 // Light rows in the partition's step order pay where a wave holds four or more
-// rows (its groups then wait on their longest row); with one or two rows per
-// wave the extra index load costs more than the balance gains.
-template <typename T, int H, int D>
+// rows (its groups then wait on their longest row), and for the GATv2 score,
+// whose steps are arithmetic-heavy, already at two.  For the graph-transformer
+// score with one or two rows per wave the extra index load and the longer
+// partition cost more than the balance gains.
+template <typename T, int H, int D, int KIND = KIND_GT>
 struct SortedLight {
-    static constexpr bool value = Geo<T, H, D>::kP >= 4;
+    static constexpr bool value = Geo<T, H, D>::kP >= 4 || (KIND == KIND_GATV2 && Geo<T, H, D>::kP >= 2);
 };
 
 template <int G> struct LightTile {
@@ -586,7 +588,7 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
     // so that it is in a register when its row pointers are needed.
     auto row_at = [&](int64_t i) -> int64_t {
         const int64_t pos = i * P + g;
-        if constexpr (SortedLight<T, H, D>::value)
+        if constexpr (SortedLight<T, H, D, KIND>::value)
             return (i < it_end && pos < p.N) ? (int64_t)p.light_list[pos] : -1;
         else
             return (i < it_end && pos < p.N) ? pos : -1;
@@ -1488,7 +1490,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const size_t o_ml = off;       off = align_up(off + (size_t)caps.slots * H * sizeof(float2), 256);
     const size_t o_acc = off;      off = align_up(off + (size_t)caps.slots * H * D * sizeof(float), 256);
     const size_t o_light = off;
-    off = align_up(off + ((tiles || !SortedLight<T, H, D>::value) ? 0 : (size_t)a.N * sizeof(int32_t)), 256);
+    off = align_up(off + ((tiles || !SortedLight<T, H, D, KIND>::value) ? 0 : (size_t)a.N * sizeof(int32_t)), 256);
     const size_t ws_bytes = off;
 
     WsEntry& we = ws_entry(dev, stream);
@@ -1535,7 +1537,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
-    pp.light_list = (tiles || !SortedLight<T, H, D>::value) ? nullptr : reinterpret_cast<int32_t*>(ws + o_light);
+    pp.light_list = (tiles || !SortedLight<T, H, D, KIND>::value) ? nullptr : reinterpret_cast<int32_t*>(ws + o_light);
     pp.step = Gm::kU;
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
     ph.mark(1, stream);  // the attention phase includes the tile kernel
