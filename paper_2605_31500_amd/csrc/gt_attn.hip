@@ -281,9 +281,19 @@ __device__ __forceinline__ float lse_of(float m, float l) {
 // for any slope s): a holds the lane's slice of a(1+s)/2 and a2 of a(1-s)/2,
 // so an element costs one add and two FMAs (|x| is a free operand modifier)
 // instead of a compare, a select and a multiply more.
+// Entries per step of a row: the geometry's step for the graph-transformer
+// score, half of it (at least 2) for the GATv2 score, whose steps are
+// arithmetic-heavy: a shorter step spends less on the padding of short rows.
+template <typename T, int H, int D, int KIND>
+struct StepOf {
+    static constexpr int kU = Geo<T, H, D>::kU;
+    static constexpr int value = (KIND == KIND_GATV2 && kU >= 4) ? kU / 2 : kU;
+};
+
 template <typename T, int H, int D, int KIND = KIND_GT>
 struct RowState {
     using Gm = Geo<T, H, D>;
+    static constexpr int kU = StepOf<T, H, D, KIND>::value;
     static constexpr bool kGat = KIND == KIND_GATV2;
     // bf16 graph-transformer rows: scores are bf16 dot2 on the raw Q and K
     // pairs, and P*V pairs two entries: their weights are rounded to one bf16
@@ -295,7 +305,7 @@ struct RowState {
     // 2^-9 * sum_e p_e |v_e| / sum_e p_e.  (GATv2 widens its gathered rows for
     // the score anyway, and reusing them for P*V measured faster than pairs.)
     static constexpr bool kDot2 = std::is_same<T, bf16_tag>::value && !kGat;
-    static_assert(!kDot2 || Gm::kU % 2 == 0, "dot2 pairs entries");
+    static_assert(!kDot2 || kU % 2 == 0, "dot2 pairs entries");
     float q[Gm::kNV][Gm::kEPV];
     float a[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
     float a2[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
@@ -339,14 +349,14 @@ struct RowState {
     // Loads of one step: the K and V rows (GATv2: the R rows) of U entries,
     // 16 bytes per lane each.
     struct Batch {
-        uint4 k[Gm::kU][Gm::kNV];
-        uint4 v[kGat ? 1 : Gm::kU][Gm::kNV];
+        uint4 k[kU][Gm::kNV];
+        uint4 v[kGat ? 1 : kU][Gm::kNV];
     };
 
     __device__ __forceinline__ void issue(const char* __restrict__ Kb, const char* __restrict__ Vb,
-                                          const int32_t (&j)[Gm::kU], int lig, Batch& bt) const {
+                                          const int32_t (&j)[kU], int lig, Batch& bt) const {
 #pragma unroll
-        for (int u = 0; u < Gm::kU; ++u) {
+        for (int u = 0; u < kU; ++u) {
             const int64_t off = (int64_t)j[u] * Gm::kRowBytes + lig * 16;
 #pragma unroll
             for (int k = 0; k < Gm::kNV; ++k) {
@@ -403,7 +413,7 @@ struct RowState {
         // subtraction of the running max would give the maximal entry a weight
         // of 2^(rounding error) instead of exactly 1.
 #pragma clang fp contract(off)
-        constexpr int U = Gm::kU;
+        constexpr int U = kU;
         float s[U][Gm::kNV];
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -452,7 +462,7 @@ struct RowState {
     }
 
     __device__ __forceinline__ void step(const char* __restrict__ Kb, const char* __restrict__ Vb,
-                                         const int32_t (&j)[Gm::kU], int nvalid, int lig, float c) {
+                                         const int32_t (&j)[kU], int nvalid, int lig, float c) {
         Batch bt;
         issue(Kb, Vb, j, lig, bt);
         consume(bt, nvalid, c);
@@ -515,7 +525,7 @@ template <typename T, int H, int D, int KIND>
 __device__ __forceinline__ void wave_segment(const AttnParams& p, int64_t row, int64_t b, int64_t e,
                                              int32_t slot, int32_t* __restrict__ tile, int lane) {
     using Gm = Geo<T, H, D>;
-    constexpr int U = Gm::kU, P = Gm::kP, G = Gm::kG;
+    constexpr int U = RowState<T, H, D, KIND>::kU, P = Gm::kP, G = Gm::kG;
     const int g = lane / G, lig = lane % G;
     RowState<T, H, D, KIND> st;
     st.begin(p.Q, row, lig, p.att, p.slope);
@@ -573,8 +583,9 @@ __device__ __forceinline__ void light_rows(const AttnParams& p, int64_t it, int6
                                            int64_t stride, int g, int lig,
                                            int32_t* __restrict__ gtile) {
     using Gm = Geo<T, H, D>;
-    constexpr int U = Gm::kU, G = Gm::kG, P = Gm::kP;
+    constexpr int U = RowState<T, H, D, KIND>::kU, G = Gm::kG, P = Gm::kP;
     constexpr int R = LightTile<G>::kR, TE = LightTile<G>::kEntries;
+    static_assert(TE % U == 0, "index tiles hold whole steps");
     // entries [tb, tb + TE) of a row ending at ce (clamped to its last entry)
     auto load_tile = [&](int64_t tb, int64_t ce, int32_t (&v)[R]) {
 #pragma unroll
@@ -1538,7 +1549,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
     pp.light_list = (tiles || !SortedLight<T, H, D, KIND>::value) ? nullptr : reinterpret_cast<int32_t*>(ws + o_light);
-    pp.step = Gm::kU;
+    pp.step = RowState<T, H, D, KIND>::kU;
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
     ph.mark(1, stream);  // the attention phase includes the tile kernel
     if constexpr (kTileShape) {
