@@ -281,13 +281,15 @@ __device__ __forceinline__ float lse_of(float m, float l) {
 // for any slope s): a holds the lane's slice of a(1+s)/2 and a2 of a(1-s)/2,
 // so an element costs one add and two FMAs (|x| is a free operand modifier)
 // instead of a compare, a select and a multiply more.
-// Entries per step of a row: the geometry's step for the graph-transformer
-// score, half of it (at least 2) for the GATv2 score, whose steps are
-// arithmetic-heavy: a shorter step spends less on the padding of short rows.
+// Entries per step of a row: the geometry's step, halved (8 -> 4) where short
+// rows dominate the work of a step: for the GATv2 score, whose steps are
+// arithmetic-heavy, and for rows narrow enough that a wave holds four or more
+// of them.  A shorter step spends less on the padding of short rows and holds
+// fewer registers.
 template <typename T, int H, int D, int KIND>
 struct StepOf {
     static constexpr int kU = Geo<T, H, D>::kU;
-    static constexpr int value = (KIND == KIND_GATV2 && kU >= 4) ? kU / 2 : kU;
+    static constexpr int value = ((KIND == KIND_GATV2 || Geo<T, H, D>::kP >= 4) && kU >= 8) ? kU / 2 : kU;
 };
 
 template <typename T, int H, int D, int KIND = KIND_GT>
@@ -782,7 +784,7 @@ gt_tile_kernel(TileParams p) {
     using Gm = Geo<bf16_tag, H, D>;
     using L = TileLds<H, D>;
     constexpr int HD = H * D;
-    constexpr int G = Gm::kG, P = Gm::kP, U = Gm::kU;
+    constexpr int G = Gm::kG, P = Gm::kP, U = RowState<bf16_tag, H, D>::kU;
     static_assert(HD <= 128 && D % 32 == 0, "tile path shapes");
     __shared__ __attribute__((aligned(16))) L lds;
 
