@@ -1105,7 +1105,9 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     if (p.light_list) {
         // Light rows of this block in descending step count (a counting sort in
         // LDS), so the lane groups of a wave take rows of similar length and a
-        // wave does not wait on one long row among short ones.  The order within
+        // wave does not wait on one long row among short ones: the degree
+        // bucketing of the degree-aware mapping (Appendix B.1), applied to the
+        // rows that share a wavefront.  The order within
         // a step class is arbitrary; every row is computed on its own, so the
         // results do not depend on it.  Positions after the block's light rows
         // hold -1.
