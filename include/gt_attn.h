@@ -32,8 +32,8 @@
  * Ownership and memory: every pointer argument is DEVICE memory owned by the
  * caller; the library neither frees nor retains it past the enqueued work.
  * `out` must not overlap Q, K or V.  Q, K, V and out must be 16-byte aligned.
- * Workspace (degree-bin lists and partial softmax states of split rows) is
- * owned by the library: one buffer per (device, stream), allocated
+ * Workspace (degree-bin lists, the light-row order of narrow-row shapes and
+ * partial softmax states of split rows) is owned by the library: one buffer per (device, stream), allocated
  * stream-ordered (hipMallocAsync) by the first call on that stream and grown
  * when a later call needs more, so steady-state calls allocate nothing.  The
  * buffers live until gt_workspace_release() or process exit.  Calls on one
