@@ -285,6 +285,46 @@ def run_hd_sweep(args, gt, torch, to_device, synth) -> int:
     return 0
 
 
+SIZE_SWEEP_N = (16_384, 65_536, 169_343, 524_288, 2_097_152, 8_388_608)
+
+
+def run_size_sweep(args, gt, torch, to_device, synth) -> int:
+    """The bench workload's graph family (the power-law in-degree law of the
+    arxiv-shaped graph, fp32 4x32 features) at sizes from 16K to 8.4M nodes:
+    where the attention forward leaves the latency-bound regime and how close
+    it stays to the HBM roof as K and V outgrow the Infinity Cache; one JSON
+    line per size."""
+    H, D = 4, 32
+    for N in SIZE_SWEEP_N:
+        rowptr, colidx = synth.chung_lu_graph(0, N)  # seed 0: N = 169,343 is the bench graph
+        E = int(rowptr[-1])
+        Q, K, V = synth.features(0, N, H, D, "f32")
+        rp, ci, q, k, v = (to_device(a) for a in (rowptr, colidx, Q, K, V))
+        del Q, K, V
+        out = torch.empty_like(q)
+        scale = 1.0 / D ** 0.5
+        step = lambda: gt.gt_attn_fwd_ex(rp, ci, q, k, v, out, scale)
+        ms = _time_calls(torch, step, args.steps)
+        gt.gt_profile_enable(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        phase_ms, calls = gt.gt_profile_collect()
+        gt.gt_profile_enable(False)
+        kern_ms = phase_ms[1] / calls
+        R = H * D * 4
+        mbytes = 8 * (N + 1) + 4 * E + N * R + 2 * E * R + N * R
+        print(json.dumps({"sweep": "graph size", "family": "chung-lu power law (arxiv degree law)", "N": N,
+                          "E": E, "H": H, "D": D, "dtype": "f32", "kv_bytes": 2 * N * R,
+                          "ms_per_call": round(ms, 5), "GEdges_per_s": round(E / (ms * 1e-3) / 1e9, 4),
+                          "attention_kernel_ms": round(kern_ms, 5),
+                          "model_GBps": round(mbytes / (kern_ms * 1e-3) / 1e9, 1),
+                          "frac_of_8TBps": round(mbytes / (kern_ms * 1e-3) / 8e12, 4)}), flush=True)
+        del rp, ci, q, k, v, out
+        torch.cuda.empty_cache()
+    return 0
+
+
 def gatv2_attention_vector(w, seed: int):
     import math
     import synth
@@ -502,6 +542,8 @@ def main() -> int:
     ap.add_argument("--ablate-degree", action="store_true",
                     help="time degree-aware versus degree-agnostic work allocation")
     ap.add_argument("--ablate-configs", default="1,2,3,4", help="graphs of the ablation (indices)")
+    ap.add_argument("--size-sweep", action="store_true",
+                    help="the bench graph family at 16K..8.4M nodes (fp32 4x32), one line per size")
     ap.add_argument("--hd-sweep", action="store_true",
                     help="time the attention forward over the paper's (H, D) grid on --config's graph")
     ap.add_argument("--sweep-dtype", choices=["f32", "bf16"], default="f32",
@@ -534,6 +576,8 @@ def main() -> int:
         return run_study(args, gt, torch, to_device, synth)
     if args.ablate_degree:
         return run_ablation(args, gt, torch, to_device, synth)
+    if args.size_sweep:
+        return run_size_sweep(args, gt, torch, to_device, synth)
     if args.hd_sweep:
         return run_hd_sweep(args, gt, torch, to_device, synth)
     w = synth.config(args.config)
