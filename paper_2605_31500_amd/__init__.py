@@ -203,6 +203,8 @@ def gt_dot_aggr(rowptr, colidx, X, out, mapping="feature", load_bytes=16, stream
             raise ValueError(name + " must be a contiguous device tensor")
     if any(t.device != X.device for t in (rowptr, colidx, out)):
         raise ValueError("all tensors must be on one device")
+    if rowptr.dtype != torch.int64 or colidx.dtype != torch.int32:
+        raise TypeError("rowptr must be int64 and colidx int32")
     if X.dtype != torch.float32 or out.dtype != torch.float32 or X.dim() != 2:
         raise TypeError("X must be float32 [N, F] and out float32 [N]")
     N, F = X.shape
@@ -287,6 +289,15 @@ def attention(rowptr, colidx, Q, K, V, scale=None, tuning=None, out=None, stream
 
 def gt_csr_validate(rowptr, colidx, stream=None) -> bool:
     """Device-side CSR structure check (synchronous)."""
+    for name, t in (("rowptr", rowptr), ("colidx", colidx)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(name + " must be a contiguous device tensor")
+    if colidx.device != rowptr.device:
+        raise ValueError("all tensors must be on one device")
+    if rowptr.dtype != torch.int64 or colidx.dtype != torch.int32:
+        raise TypeError("rowptr must be int64 and colidx int32")
+    if rowptr.numel() < 1:
+        raise ValueError("rowptr must have N+1 >= 1 entries")
     valid = ctypes.c_int32(0)
     _check(load_library().gt_csr_validate(_ptr(rowptr), _ptr(colidx), rowptr.numel() - 1,
                                           colidx.numel(), ctypes.byref(valid),

@@ -253,6 +253,39 @@ def test_errors_raise():
     assert e.value.status == m.GT_ERROR_INVALID_VALUE
 
 
+def test_binding_rejects_wrong_index_tensors():
+    """Index tensors of the wrong dtype or on the host are refused before any
+    launch (an int32 rowptr read as int64 would run past its end)."""
+    m = gt()
+    rp32 = torch.zeros(11, dtype=torch.int32, device="cuda")
+    rp = torch.zeros(11, dtype=torch.int64, device="cuda")
+    ci = torch.zeros(0, dtype=torch.int32, device="cuda")
+    ci64 = torch.zeros(0, dtype=torch.int64, device="cuda")
+    X = torch.zeros(10, 32, device="cuda")
+    s = torch.zeros(10, device="cuda")
+    with pytest.raises(TypeError):
+        m.gt_dot_aggr(rp32, ci, X, s)
+    with pytest.raises(TypeError):
+        m.gt_dot_aggr(rp, ci64, X, s)
+    with pytest.raises(TypeError):
+        m.gt_csr_validate(rp32, ci)
+    with pytest.raises(TypeError):
+        m.gt_csr_validate(rp, ci64)
+    with pytest.raises(ValueError):
+        m.gt_csr_validate(rp.cpu(), ci)
+    with pytest.raises(ValueError):
+        m.gt_csr_validate(rp[:0], ci)
+    z = torch.zeros(10, 4, 32, device="cuda")
+    with pytest.raises(TypeError):
+        m.gt_attn_fwd(rp32, ci, z, z, z, z.clone(), 0.1)
+    with pytest.raises(ValueError):
+        m.gt_attn_fwd(rp.cpu(), ci, z, z, z, z.clone(), 0.1)
+    assert m.gt_csr_validate(rp, ci)  # N = 10 empty rows is a valid structure
+    m.gt_dot_aggr(rp, ci, X, s)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(s).item() == 0
+
+
 def test_profiler_counts_calls():
     m = gt()
     N, H, D = 3000, 4, 32
