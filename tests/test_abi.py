@@ -183,3 +183,23 @@ def test_bwd_host_validation(lib, kw, status):
 
 def test_bwd_empty_graph_is_a_no_op(lib):
     assert call_bwd(lib, N=0, E=0) == 0
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """Without the built library the binding raises; it has no other path."""
+    import paper_2605_31500_amd as gt
+    monkeypatch.setattr(gt, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        gt.load_library(str(tmp_path / "libgtattn.so"))
+
+
+def test_product_sources_do_not_reach_the_oracle():
+    """The package (binding and HIP sources) neither imports nor names the
+    test oracle, so no product call can be served by it."""
+    pkg = os.path.join(ROOT, "paper_2605_31500_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\boracle\b", text), os.path.join(dirpath, f)
+    assert not re.search(r"\boracle\b", open(HEADER).read())
