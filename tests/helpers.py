@@ -33,6 +33,24 @@ def gate_error(x, ref, absagg) -> float:
     return float(np.max(np.abs(x - ref) / denom))
 
 
+def score_rounding_bound(rowptr, colidx, Q, K, scale) -> np.ndarray:
+    """Per (row, head): the largest bound on the absolute rounding error of a
+    computed score of the row, D * 2^-24 * scale * sum_d |q_d k_d| (the
+    standard bound for a D-term fp32 dot product, plus the scaling).  Q, K:
+    float32 or bf16 bits.  Rows without entries get 0."""
+    N, H, D = Q.shape
+    widen = lambda x: bf16_bits_to_f32(x) if x.dtype == np.uint16 else x
+    q, k = np.abs(widen(Q).astype(np.float64)), np.abs(widen(K).astype(np.float64))
+    deg = np.diff(rowptr)
+    dst = np.repeat(np.arange(N), deg)
+    per_entry = np.einsum("ehd,ehd->eh", q[dst], k[colidx]) * D * 2.0 ** -24 * scale
+    bound = np.zeros((N, H))
+    nz = deg > 0
+    if per_entry.size:
+        bound[nz] = np.maximum.reduceat(per_entry, rowptr[:-1][nz], axis=0)
+    return bound
+
+
 def bf16_bits_to_f32(bits) -> np.ndarray:
     return (np.asarray(bits).astype(np.uint32) << 16).view(np.float32)
 

@@ -10,7 +10,8 @@ import pytest
 
 import oracle
 import synth
-from tests.helpers import (TOL_BF16, TOL_F32, gate_error, run_gpu_fwd_bwd, sample_rows)
+from tests.helpers import (TOL_BF16, TOL_F32, gate_error, run_gpu_fwd_bwd, sample_rows,
+                           score_rounding_bound)
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +63,45 @@ def test_lse_and_backward_small(H, D, dtype, split):
     _, _, ref_lse = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, want_absagg=False)
     check_lse(got[1], ref_lse, 1e-5)
     check_grads(rowptr, colidx, Q, K, V, dO, scale, got, dtype)
+
+
+def per_node_error(x, r, scale):
+    """max over the feature axis of |x - r| / max(|r|, S): [nodes, H]."""
+    return np.max(np.abs(x - r) / np.maximum(np.maximum(np.abs(r), scale), 1e-30), axis=2)
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_backward_peaked_scores(dtype, split):
+    """Scores spread over hundreds of units (most weights underflow, one or two
+    entries carry a row).  A recomputed weight exp(s_e - lse_i) is off by at
+    most the rounding errors of s_e and of lse_i, and Delta_i = <out_i, dout_i>
+    inherits the error of out_i, each at most the row's worst score error e_i
+    (tests.helpers.score_rounding_bound).  So dQ of row i is held to 3 e_i, and
+    dK, dV of node j to 3 max e_i over the rows i that hold j, plus the gate."""
+    N, H, D = 3000, 4, 32
+    scale = 6.0
+    rowptr, colidx = synth.ragged_graph(41, N, max_deg=40, hubs={3: 2999, 9: 1800})
+    Q, K, V = synth.features(41, N, H, D, dtype)
+    dO, _, _ = synth.features(42, N, H, D, dtype)
+    out, lse, dq, dk, dv = run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, np.float32(scale),
+                                           tuning=FORCED_SPLIT if split else None)
+    gate = tol(dtype)
+    e_row = score_rounding_bound(rowptr, colidx, Q, K, scale)
+    e_col = np.zeros_like(e_row)
+    np.maximum.at(e_col, colidx, e_row[np.repeat(np.arange(N), np.diff(rowptr))])
+    _, _, ref_lse = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, want_absagg=False)
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isneginf(lse), ~fin)
+    assert np.all(np.abs(lse[fin] - ref_lse[fin]) <= e_row[fin] + 1e-5 * np.maximum(1.0, np.abs(ref_lse[fin])))
+    rpt, cit = synth.transpose_csr(rowptr, colidx, N)
+    rq, sq = oracle.gt_attn_bwd_dq(rowptr, colidx, Q, K, V, dO, scale)
+    rk, rv, sk, sv = oracle.gt_attn_bwd_dkv(rowptr, colidx, rpt, cit, Q, K, V, dO, scale)
+    for name, x, r, sc, e in (("dQ", dq, rq, sq, e_row), ("dK", dk, rk, sk, e_col), ("dV", dv, rv, sv, e_col)):
+        assert np.all(np.isfinite(x)), name
+        err = per_node_error(x, r, sc)
+        bound = 3.0 * e + gate
+        assert np.all(err <= bound), "%s worst ratio %.3g" % (name, np.max(err / bound))
 
 
 def test_backward_deterministic():

@@ -9,8 +9,8 @@ import torch
 
 import oracle
 import synth
-from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, run_gpu, to_device,
-                           to_host_f32)
+from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, run_gpu,
+                           score_rounding_bound, to_device, to_host_f32)
 
 pytestmark = pytest.mark.gpu
 
@@ -253,27 +253,6 @@ def test_errors_raise():
     assert e.value.status == m.GT_ERROR_INVALID_VALUE
 
 
-def score_error_bound(rowptr, colidx, Q, K, scale, gate=TOL_F32):
-    """Per (row, head) bound on the output error caused by rounding the scores.
-
-    A computed score has absolute error at most D * 2^-24 * scale * sum_d |q_d k_d|
-    (the standard bound for an fp32 dot product of D terms, plus the scaling),
-    and a weight exp(s_e - m) then has relative error at most the sum of the
-    errors of s_e and m.  Output error relative to sum_e alpha_e |v_e| is thus
-    bounded by twice the largest score error of the row, plus the 1e-5 gate of
-    well-conditioned rows."""
-    N, H, D = Q.shape
-    widen = lambda x: bf16_bits_to_f32(x) if x.dtype == np.uint16 else x
-    q, k = np.abs(widen(Q).astype(np.float64)), np.abs(widen(K).astype(np.float64))
-    deg = np.diff(rowptr)
-    dst = np.repeat(np.arange(N), deg)
-    per_entry = np.einsum("ehd,ehd->eh", q[dst], k[colidx]) * D * 2.0 ** -24 * scale  # [E, H]
-    bound = np.zeros((N, H))
-    nz = deg > 0
-    bound[nz] = np.maximum.reduceat(per_entry, rowptr[:-1][nz], axis=0)
-    return 2.0 * bound + gate
-
-
 @pytest.mark.parametrize("tuning", [None, {"light_max_deg": 2, "heavy_min_deg": 6, "chunk_edges": 64}],
                          ids=["default", "forced_split"])
 @pytest.mark.parametrize("scale", [2.0, 8.0])
@@ -291,7 +270,9 @@ def test_peaked_scores(dtype, scale, tuning):
     assert np.all(np.isfinite(got))
     denom = np.maximum(np.maximum(np.abs(ref), absagg), 1e-30)
     err = np.max(np.abs(got - ref) / denom, axis=2)  # [N, H]
-    bound = score_error_bound(rowptr, colidx, Q, K, scale, TOL_F32 if dtype == "f32" else TOL_BF16)
+    # a weight exp(s_e - m) is off by at most the errors of s_e and of the running max
+    bound = (2.0 * score_rounding_bound(rowptr, colidx, Q, K, scale)
+             + (TOL_F32 if dtype == "f32" else TOL_BF16))
     assert np.all(err <= bound), "worst ratio %.3g" % np.max(err / bound)
     # the spread is real: on most rows the largest weight is above 0.9
     Qf, Kf = ((bf16_bits_to_f32(x) if dtype == "bf16" else x).astype(np.float64) for x in (Q, K))
