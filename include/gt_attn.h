@@ -108,7 +108,10 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  *                   between get one wavefront each (default 256)
  *   chunk_edges   : CSR entries per chunk of a split row, rounded up to a
  *                   multiple of 64; a row is cut into at most 32 chunks, so
- *                   very long rows get longer chunks (default 1024)
+ *                   very long rows get longer chunks (default 1024 on large
+ *                   graphs; on small graphs shorter, down to 64, so that one
+ *                   chunk's chain of dependent steps stays within about half
+ *                   the call's gather time)
  *   grid_blocks   : workgroups of the attention kernel, rounded up to a
  *                   multiple of 8 (default: about two light work items per
  *                   wavefront, within 4x..64x the resident workgroups)

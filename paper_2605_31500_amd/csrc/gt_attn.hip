@@ -1423,6 +1423,24 @@ PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
     return c;
 }
 
+// Default chunk length of split rows.  A chunk is one wavefront's chain of
+// dependent steps (P*U entries each, about one memory round trip, ~1 us), so
+// the longest chunk bounds the call from below.  On a small graph a 1024-entry
+// chunk outlasts everything else: on the arxiv-shaped power-law graph with
+// fp32 4x32 features, 16K nodes took 76 us per call at 1024 against 48 us at
+// 256, and 65K nodes 114 us against 95 us at 512.  The default keeps a chunk's
+// steps within half the time the call's gathers take at ~7 TB/s, in multiples
+// of 64, capped at 1024, the measured best on large graphs (the bench graph,
+// 169K nodes, and every larger one get 1024).
+int default_chunk(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
+    constexpr double kGatherBytesPerSecond = 7.0e12, kStepSeconds = 1.0e-6;
+    const double gather_seconds = (double)E * (double)bytes_per_entry / kGatherBytesPerSecond;
+    const double entries = 0.5 * gather_seconds / kStepSeconds * entries_per_step;
+    if (entries >= 1024.0) return 1024;
+    const int64_t c = ((int64_t)entries + kWave - 1) / kWave * kWave;
+    return (int)(c < kWave ? kWave : c);
+}
+
 int device_cus(int dev) {
     static std::atomic<int> cache[64];
     if (dev < 0 || dev >= 64) return 256;
@@ -1453,10 +1471,14 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
     // Defaults chosen by measurement on the five workload shapes (power law,
     // R-MAT, SBM, lognormal hubs): a group handles rows of up to 8 steps;
-    // rows of degree >= 256 go first, split into chunks of 1024 entries.
+    // rows of degree >= 256 go first, split into chunks of 1024 entries on
+    // large graphs, shorter ones on small graphs (default_chunk).  GATv2 takes
+    // the chunk of the graph-transformer forward of its shape: counted from
+    // its own single gather and half step, the bench graph's chunks would
+    // shrink to 384 entries, which measured 5.7 % slower there.
     int light_max = 8 * Gm::kU;
     int heavy_min = 256;
-    int chunk = 1024;
+    int chunk = default_chunk(a.E, 2 * Gm::kRowBytes, Gm::kP * StepOf<T, H, D, KIND_GT>::value);
     int grid = 0;
     int tile_min = 0;  // dense-tile windows off
     if (tu) {

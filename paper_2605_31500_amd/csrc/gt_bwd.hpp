@@ -391,7 +391,7 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
     const int light_max = 8 * Gm::kU;
     const int heavy_min = 256;
-    const int chunk = 1024;
+    const int chunk = default_chunk(a.E, 2 * Gm::kRowBytes, Gm::kP * Gm::kU);  // both passes gather two rows
     int dev = 0;
     hipError_t he = hipGetDevice(&dev);
     if (he != hipSuccess) return hip_fail(he, "hipGetDevice");

@@ -374,7 +374,7 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     using Gm = RedGeo<T, NVEC>;
     int light_max = 8 * Gm::kU;
     int heavy_min = 256;
-    int chunk = 1024;
+    int chunk = default_chunk(a.E, Gm::kRowBytes, Gm::kP * Gm::kU);
     int grid = 0;
     if (tu) {
         if (tu->light_max_deg > 0) light_max = tu->light_max_deg;
