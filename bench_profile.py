@@ -9,9 +9,9 @@ live line), once under `rocprofv3 --kernel-trace --stats`, and once under
 `rocprofv3 --pmc` per counter group (the profiler collects one group per
 pass).  `copycal` profiles a plain 1 GiB device copy with the two HBM byte
 counters; its readings calibrate FETCH_SIZE and WRITE_SIZE.  Raw output goes
-to OUT/<mode>/ (default gpurun_out/).  Every GPU run is a child process with
-its own time limit; this script never touches the GPU, and it stops at the
-first run that fails.
+to OUT/<mode>/ (default captures/, kept out of version control).  Every GPU
+run is a child process with its own time limit; this script never touches
+the GPU, and it stops at the first run that fails.
 
 summarize turns OUT/<mode>/ into profiles/<summary>.md (the commands, the
 kernel table, the calibrated HBM bytes, the L2 hit rate, LDS bank conflicts
@@ -291,7 +291,7 @@ def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("action", choices=["capture", "summarize", "list"])
     ap.add_argument("modes", nargs="*", help="capture modes (or 'all'); capture also takes 'copycal'")
-    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out"), help="raw capture directory")
+    ap.add_argument("--out", default=os.path.join(ROOT, "captures"), help="raw capture directory")
     a = ap.parse_args(argv)
     if a.action == "list":
         for m, s in CAPTURES.items():
