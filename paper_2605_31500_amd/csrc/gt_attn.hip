@@ -1472,13 +1472,16 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     // Defaults chosen by measurement on the five workload shapes (power law,
     // R-MAT, SBM, lognormal hubs): a group handles rows of up to 8 steps;
     // rows of degree >= 256 go first, split into chunks of 1024 entries on
-    // large graphs, shorter ones on small graphs (default_chunk).  GATv2 takes
-    // the chunk of the graph-transformer forward of its shape: counted from
-    // its own single gather and half step, the bench graph's chunks would
-    // shrink to 384 entries, which measured 5.7 % slower there.
+    // large graphs, shorter ones on small graphs (default_chunk).  GATv2
+    // counts its own single gather per entry but the graph-transformer step:
+    // that put its chunks at the measured optimum on the arxiv-shaped graph
+    // with 16K and 65K nodes (65K: 92.6 -> 77.5 us per call) and at 768
+    // entries on the 169K-node one (within 1 % of 1024).  Its own half step
+    // would give 384 entries there, 5.7 % slower.
     int light_max = 8 * Gm::kU;
     int heavy_min = 256;
-    int chunk = default_chunk(a.E, 2 * Gm::kRowBytes, Gm::kP * StepOf<T, H, D, KIND_GT>::value);
+    int chunk = default_chunk(a.E, (KIND == KIND_GT ? 2 : 1) * Gm::kRowBytes,
+                              Gm::kP * StepOf<T, H, D, KIND_GT>::value);
     int grid = 0;
     int tile_min = 0;  // dense-tile windows off
     if (tu) {
