@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import synth
-from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, run_gpu,
+from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, run_gpu, sample_rows,
                            score_rounding_bound, to_device, to_host_f32)
 
 pytestmark = pytest.mark.gpu
@@ -388,3 +388,30 @@ def test_step_ordered_light_rows(dtype, tuning):
     g, _ = run_gpu_gatv2(rowptr, colidx, Q, K, att, 0.2, tuning=tu)
     gref, gabs, _ = oracle.gatv2_fwd(rowptr, colidx, Q, K, att, 0.2, want_lse=False)
     assert gate_error(g, gref, gabs) <= t
+
+
+@pytest.mark.parametrize("N", [16384, 65536])
+@pytest.mark.parametrize("kind", ["gt", "gatv2"])
+def test_small_graph_short_chunks(kind, N):
+    """Small power-law graphs take short chunks for their hub rows (a few
+    hundred entries; on 16K nodes the largest hub is cut into the full 32
+    chunks): the hubs and a sample of other rows match the oracle under the
+    default partition."""
+    import paper_2605_31500_amd as m
+    H, D = 4, 32
+    rowptr, colidx = synth.chung_lu_graph(0, N)
+    Q, K, V = synth.features(0, N, H, D, "f32")
+    rows = sample_rows(rowptr, 200, 40, seed=N)
+    assert np.diff(rowptr).max() > 32 * 192  # the largest hub has more entries than 32 short chunks hold
+    dt = [to_device(x) for x in (rowptr, colidx, Q, K)]
+    out = torch.empty_like(dt[2])
+    if kind == "gt":
+        m.gt_attn_fwd_ex(*dt, to_device(V), out, 0.25)
+        ref, absagg, _ = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, 0.25, rows=rows, want_lse=False)
+    else:
+        att = synth.normal(N, synth.STREAM_EXTRA + 9, (H, D), 1.0 / math.sqrt(D), "f32")
+        m.gt_gatv2_fwd(dt[0], dt[1], dt[2], dt[3], to_device(att), 0.2, out)
+        ref, absagg, _ = oracle.gatv2_fwd(rowptr, colidx, Q, K, att, 0.2, rows=rows, want_lse=False)
+    torch.cuda.synchronize()
+    got = to_host_f32(out)[rows]
+    assert gate_error(got, ref, absagg) <= TOL_F32
