@@ -38,7 +38,9 @@ CAPTURES = {
     "gt": dict(args=[], kernels=["gt_attn_kernel"], key="{w}",
                title="Graph-transformer attention forward", model=GT_MODEL,
                summary="gt_attn_kernel_{w}"),
-    "gatv2": dict(args=["--gatv2"], kernels=["gt_attn_kernel"], key="{w}:gatv2",
+    "c1": dict(args=["--config", "1"], kernels=["gt_attn_kernel"], key="{w}",
+               title="Graph-transformer attention forward", model=GT_MODEL, summary="gt_attn_kernel_{w}"),
+    "gatv2": dict(args=["--gatv2", "--config", "1"], kernels=["gt_attn_kernel"], key="{w}:gatv2",
                   title="GATv2 attention forward",
                   model="per-edge model: rowptr + colidx + L + R per CSR entry + out + attention vector",
                   summary="gt_attn_kernel_gatv2_{w}"),
@@ -51,10 +53,10 @@ CAPTURES = {
     "c3t": dict(args=["--config", "3", "--dense-tiles", "256"], kernels=["gt_tile_kernel", "gt_attn_kernel"],
                 key=None, title="Graph-transformer attention forward, dense tiles", model=GT_MODEL,
                 summary="gt_tile_kernel_{w}"),
-    "bwd": dict(args=["--backward"], kernels=["gt_bwd_kernel"], key="{w}:backward",
+    "bwd": dict(args=["--backward", "--config", "1"], kernels=["gt_bwd_kernel"], key="{w}:backward",
                 title="Graph-transformer attention backward (both passes)", model="backward per-edge model",
                 summary="gt_bwd_kernel_{w}"),
-    "reduce": dict(args=["--reduce", "min"], kernels=["gt_reduce_kernel"], key="{g}:reduce-min-f512",
+    "reduce": dict(args=["--reduce", "min", "--config", "1"], kernels=["gt_reduce_kernel"], key="{g}:reduce-min-f512",
                    title="Segment min aggregation",
                    model="rowptr + colidx + one gathered row per entry + out + int32 sources",
                    summary="gt_reduce_kernel_{w}"),

@@ -62,12 +62,19 @@ def _load():
         L.gt_oracle_dot_aggr.restype = ctypes.c_int
         L.gt_oracle_threads.argtypes = []
         L.gt_oracle_threads.restype = ctypes.c_int
+        L.gt_oracle_set_threads.argtypes = [ctypes.c_int]
+        L.gt_oracle_set_threads.restype = None
         _lib = L
     return _lib
 
 
 def threads() -> int:
     return int(_load().gt_oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads of later oracle calls in this process (n >= 1)."""
+    _load().gt_oracle_set_threads(int(n))
 
 
 def _ptr(a):

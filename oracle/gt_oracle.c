@@ -57,6 +57,15 @@ int gt_oracle_threads(void) {
 #endif
 }
 
+/* Threads of later parallel regions (n >= 1); used to time single-threaded runs. */
+void gt_oracle_set_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /*
  * Computes rows rows[0..nrows) (all rows 0..N-1 when rows == NULL, with
  * nrows == N).  Results for the r-th requested row go to out[r,h,d],

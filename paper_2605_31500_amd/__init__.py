@@ -287,6 +287,25 @@ def attention(rowptr, colidx, Q, K, V, scale=None, tuning=None, out=None, stream
     return (out, lse) if return_lse else out
 
 
+def from_numpy(a):
+    """numpy array -> contiguous tensor on the current device; uint16 arrays
+    (bf16 bit patterns) become torch.bfloat16 with the same bits."""
+    import numpy as np
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(a).cuda()
+
+
+def to_numpy_f32(t):
+    """Device tensor -> float32 numpy array (bf16 widened exactly)."""
+    import numpy as np
+    if t.dtype == torch.bfloat16:
+        bits = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return (bits.astype(np.uint32) << 16).view(np.float32)
+    return t.cpu().numpy()
+
+
 def gt_csr_validate(rowptr, colidx, stream=None) -> bool:
     """Device-side CSR structure check (synchronous)."""
     for name, t in (("rowptr", rowptr), ("colidx", colidx)):
@@ -318,5 +337,5 @@ def gt_profile_collect():
 
 
 def gt_workspace_release() -> None:
-    """Free the library's cached per-stream workspaces (synchronises devices)."""
+    """Return the unused memory of the library's workspace pools to the devices."""
     _check(load_library().gt_workspace_release())

@@ -12,6 +12,7 @@ relative error.
 """
 from __future__ import annotations
 
+import functools
 import math
 import os
 from fractions import Fraction
@@ -106,22 +107,55 @@ def load_worked_example(name: str = "worked_example.txt") -> dict:
     return rows
 
 
+# ------------------------------------------------------- workloads, row blocks
+
+@functools.lru_cache(maxsize=None)
+def _graph(name: str):
+    import synth
+    return synth.graph(name)
+
+
+@functools.lru_cache(maxsize=None)
+def workload(idx: int):
+    """synth.config(idx), built once per test session (workloads 2 and 5 share
+    one generated graph).  Callers must not modify the arrays."""
+    import synth
+    return synth.config_from_graph(idx, *_graph(synth.GRAPH_OF[idx]))
+
+
+def row_blocks(N: int, elems_per_row: int, budget: int = 1 << 25):
+    """Consecutive (lo, hi) row ranges covering [0, N), about `budget` output
+    elements each: the oracle runs block by block, so that its float64 outputs
+    stay a few hundred MB whatever the graph size."""
+    step = max(1, budget // max(1, elems_per_row))
+    for lo in range(0, N, step):
+        yield lo, min(N, lo + step)
+
+
+def fwd_gate_error_all_rows(w, got) -> float:
+    """Gate error of a forward output (float32 [N, H, D]) against the oracle on
+    every row of workload-like `w` (rowptr, colidx, Q, K, V, scale, N, H, D)."""
+    import oracle
+    err = 0.0
+    for lo, hi in row_blocks(w.N, w.H * w.D):
+        ref, absagg, _ = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale,
+                                           rows=np.arange(lo, hi, dtype=np.int64), want_lse=False)
+        err = max(err, gate_error(got[lo:hi], ref, absagg))
+    return err
+
+
 # ------------------------------------------------------------ device helpers
 
 def to_device(a):
     """numpy -> torch CUDA tensor; uint16 arrays (bf16 bits) become torch.bfloat16."""
-    import torch
-    if a.dtype == np.uint16:
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
-    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    import paper_2605_31500_amd as gt
+    return gt.from_numpy(a)
 
 
 def to_host_f32(t) -> np.ndarray:
     """torch CUDA tensor -> float32 numpy (bf16 widened exactly)."""
-    import torch
-    if t.dtype == torch.bfloat16:
-        return bf16_bits_to_f32(t.view(torch.int16).cpu().numpy().view(np.uint16))
-    return t.cpu().numpy()
+    import paper_2605_31500_amd as gt
+    return gt.to_numpy_f32(t)
 
 
 def run_gpu(rowptr, colidx, Q, K, V, scale, tuning=None, stream=None):
@@ -131,6 +165,19 @@ def run_gpu(rowptr, colidx, Q, K, V, scale, tuning=None, stream=None):
     dt = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
     out = torch.empty_like(dt[2])
     gt.gt_attn_fwd_ex(*dt, out, scale, tuning=tuning, stream=stream)
+    torch.cuda.synchronize()
+    return to_host_f32(out)
+
+
+def run_gpu_bare(rowptr, colidx, Q, K, V, scale, stream=None):
+    """One call of the contract entry point of the feature dtype, gt_attn_fwd
+    (fp32) or gt_attn_fwd_bf16, through the C ABI; float32 host output."""
+    import torch
+    import paper_2605_31500_amd as gt
+    dt = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    out = torch.empty_like(dt[2])
+    fn = gt.gt_attn_fwd if Q.dtype == np.float32 else gt.gt_attn_fwd_bf16
+    fn(*dt, out, scale, stream=stream)
     torch.cuda.synchronize()
     return to_host_f32(out)
 

@@ -82,3 +82,23 @@ def test_paper_context_is_labelled():
     # the paper's ratios are quoted with their hardware and quantity, never as a target
     for key, ctx in bench.PAPER_CONTEXT.items():
         assert "A100" in ctx["hardware"] and "t_DGL / t" in ctx["quantity"], key
+
+
+def test_cpu_baseline_parity_and_single_thread():
+    """The CPU-baseline leg: its first oracle pass over all rows gives the gate
+    error of a GPU output; here the output is the oracle's own, rounded to
+    fp32, so the error is the fp32 rounding (<= 2^-24) and a planted error in
+    one element is found."""
+    import oracle
+    w = synth.config(0)
+    ref, _, _ = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_absagg=False,
+                                   want_lse=False)
+    got = ref.astype(np.float32)
+    res = bench.cpu_baseline(w, 0.05, got=got, single_thread_configs=(0,))
+    assert 0 <= res["gate_error"] <= 2.0 ** -24
+    cb = res["cpu_baseline"]
+    assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1
+    assert cb["single_thread"]["er-2k-h1d32-f32"]["seconds"] > 0
+    assert oracle.threads() == cb["cores"]  # restored after the single-thread run
+    got[123, 0, 7] += 1.0
+    assert bench.cpu_baseline(w, 0.0, got=got)["gate_error"] > 0.1

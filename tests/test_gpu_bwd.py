@@ -10,8 +10,8 @@ import pytest
 
 import oracle
 import synth
-from tests.helpers import (TOL_BF16, TOL_F32, gate_error, run_gpu_fwd_bwd, sample_rows,
-                           score_rounding_bound)
+from tests.helpers import (TOL_BF16, TOL_F32, gate_error, row_blocks, run_gpu_fwd_bwd,
+                           score_rounding_bound, workload)
 
 pytestmark = pytest.mark.gpu
 
@@ -136,25 +136,34 @@ def test_lse_tile_mode():
     check_lse(got[1], ref_lse, 4e-3)  # tile weights are rounded to bf16
 
 
-def test_full_config_power_law_all_rows():
-    w = synth.config(1)
-    dO, _, _ = synth.features(37, w.N, w.H, w.D, w.dtype)
-    got = run_gpu_fwd_bwd(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale)
-    _, _, ref_lse = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_absagg=False)
-    check_lse(got[1], ref_lse, 1e-5)
-    check_grads(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale, got, w.dtype)
+def check_grads_all(w, dO, got):
+    """lse on every row, dQ on every row and dK, dV on every column, the oracle
+    taken in row (column) blocks."""
+    out, lse, dq, dk, dv = got
+    rpt, cit = synth.transpose_csr(w.rowptr, w.colidx, w.N)
+    for name, x in (("dQ", dq), ("dK", dk), ("dV", dv)):
+        assert np.all(np.isfinite(x)), name
+    errs = {"dQ": 0.0, "dK": 0.0, "dV": 0.0}
+    for lo, hi in row_blocks(w.N, 2 * w.H * w.D):
+        idx = np.arange(lo, hi, dtype=np.int64)
+        _, _, ref_lse = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, rows=idx,
+                                           want_absagg=False)
+        check_lse(lse[lo:hi], ref_lse, 1e-5)
+        rq, sq = oracle.gt_attn_bwd_dq(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale, rows=idx)
+        errs["dQ"] = max(errs["dQ"], gate_error(dq[lo:hi], rq, sq))
+        rk, rv, sk, sv = oracle.gt_attn_bwd_dkv(w.rowptr, w.colidx, rpt, cit, w.Q, w.K, w.V, dO, w.scale,
+                                                cols=idx)
+        errs["dK"] = max(errs["dK"], gate_error(dk[lo:hi], rk, sk))
+        errs["dV"] = max(errs["dV"], gate_error(dv[lo:hi], rv, sv))
+    print("gate errors", {k: "%.3g" % v for k, v in errs.items()}, flush=True)
+    for name, err in errs.items():
+        assert err <= tol(w.dtype), "%s gate error %.3g" % (name, err)
 
 
-@pytest.mark.parametrize("idx", [2, 3, 4])
-def test_full_config_sampled(idx):
-    w = synth.config(idx)
-    print("config", idx, w.name, flush=True)
-    dO, _, _ = synth.features(38, w.N, w.H, w.D, w.dtype)
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
+def test_full_config_all_rows_and_columns(idx):
+    w = workload(idx)
+    print("config", idx, w.name, "N", w.N, "E", w.E, flush=True)
+    dO, _, _ = synth.features(37 if idx == 1 else 38, w.N, w.H, w.D, w.dtype)
     got = run_gpu_fwd_bwd(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale)
-    rows = sample_rows(w.rowptr, n_random=1500, n_top=32)
-    rpt, _ = synth.transpose_csr(w.rowptr, w.colidx, w.N)
-    cols = sample_rows(rpt, n_random=1500, n_top=32, seed=1)
-    _, _, ref_lse = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, rows=rows,
-                                       want_absagg=False)
-    check_lse(got[1][rows], ref_lse, 1e-5)
-    check_grads(w.rowptr, w.colidx, w.Q, w.K, w.V, dO, w.scale, got, w.dtype, rows=rows, cols=cols)
+    check_grads_all(w, dO, got)

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from tests.helpers import sample_rows, to_device
+from tests.helpers import to_device, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -78,12 +78,11 @@ def test_dot_aggr_integer_inputs_are_exact(mapping, load_bytes):
 @pytest.mark.parametrize("mapping,load_bytes", VARIANTS)
 def test_dot_aggr_study_graph(mapping, load_bytes, order):
     # the power-law bench graph at F = 128 under the study's three orders
-    w = synth.config(1)
+    w = workload(1)
     X = synth.normal(1, synth.STREAM_Q, (w.N, 128), 1.0, "f32")
     rowptr, colidx = w.rowptr, w.colidx
     if order != "original":
         perm = synth.random_order(1, w.N) if order == "random" else synth.rcm_order(rowptr, colidx)
         rowptr, colidx = synth.permute_graph(rowptr, colidx, perm)
         X = np.ascontiguousarray(X[perm])
-    rows = sample_rows(rowptr, n_random=4000, n_top=64)
-    check(rowptr, colidx, X, mapping, load_bytes, rows=rows)
+    check(rowptr, colidx, X, mapping, load_bytes)

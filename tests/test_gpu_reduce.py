@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from tests.helpers import sample_rows, to_device
+from tests.helpers import row_blocks, to_device, workload
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +50,16 @@ def check(rowptr, colidx, X, dtype, op, tuning=None, rows=None):
         bits, arg = bits[rows], arg[rows]
     assert np.array_equal(bits, oracle_bits(ref, dtype)), "values differ"
     assert np.array_equal(arg, ref_arg), "selected sources differ"
+
+
+def check_all_rows(rowptr, colidx, X, dtype, op):
+    """Every row, the oracle taken in row blocks."""
+    bits, arg = run_gpu_reduce(rowptr, colidx, X, op)
+    N = X.shape[0]
+    for lo, hi in row_blocks(N, X.shape[1], budget=1 << 26):
+        ref, ref_arg = oracle.segment_reduce(rowptr, colidx, X, op, rows=np.arange(lo, hi, dtype=np.int64))
+        assert np.array_equal(bits[lo:hi], oracle_bits(ref, dtype)), "values differ in rows [%d, %d)" % (lo, hi)
+        assert np.array_equal(arg[lo:hi], ref_arg), "selected sources differ in rows [%d, %d)" % (lo, hi)
 
 
 @pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
@@ -112,28 +122,18 @@ def test_reduce_empty_graph_and_single_row():
     assert np.array_equal(bits[0], X[0].view(np.int32)) and np.all(arg == 0)
 
 
-@pytest.mark.parametrize("idx", [0, 1])
+@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4, 5])
 def test_reduce_full_config_all_rows(idx):
-    w = synth.config(idx)
+    w = workload(idx)
     print("config", idx, w.name, "N", w.N, "E", w.E, flush=True)
     X = np.ascontiguousarray(w.Q.reshape(w.N, w.H * w.D))
     for op in ("min", "max"):
-        check(w.rowptr, w.colidx, X, w.dtype, op)
-
-
-@pytest.mark.parametrize("idx", [2, 3, 4])
-def test_reduce_full_config_sampled_rows(idx):
-    w = synth.config(idx)
-    print("config", idx, w.name, "N", w.N, "E", w.E, flush=True)
-    X = np.ascontiguousarray(w.Q.reshape(w.N, w.H * w.D))
-    rows = sample_rows(w.rowptr, n_random=3000, n_top=64)
-    check(w.rowptr, w.colidx, X, w.dtype, "min", rows=rows)
+        check_all_rows(w.rowptr, w.colidx, X, w.dtype, op)
 
 
 def test_reduce_bench_workload_f512():
     # the configuration the reduction bench times: the power-law graph with
     # 512 fp32 features per node (the paper's hidden size for this family)
-    w = synth.config(1)
+    w = workload(1)
     X = features(1, w.N, 512, "f32")
-    rows = sample_rows(w.rowptr, n_random=5000, n_top=64)
-    check(w.rowptr, w.colidx, X, "f32", "min", rows=rows)
+    check_all_rows(w.rowptr, w.colidx, X, "f32", "min")
