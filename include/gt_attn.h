@@ -32,12 +32,15 @@
  * Ownership and memory: every pointer argument is DEVICE memory owned by the
  * caller; the library neither frees nor retains it past the enqueued work.
  * `out` must not overlap Q, K or V.  Q, K, V and out must be 16-byte aligned.
- * Workspace (degree-bin lists, the light-row order of narrow-row shapes and
- * partial softmax states of split rows) is owned by the library: one buffer per (device, stream), allocated
- * stream-ordered (hipMallocAsync) by the first call on that stream and grown
- * when a later call needs more, so steady-state calls allocate nothing.  The
- * buffers live until gt_workspace_release() or process exit.  Calls on one
- * stream (from any host threads) are serialised by the library.
+ * Workspace (degree-bin lists, the light-row order of narrow-row shapes,
+ * partial softmax states of split rows and the work-list counters) is owned
+ * by the library and private to each call: it is allocated from the
+ * library's memory pool of the device with hipMallocFromPoolAsync on
+ * `stream` and freed with hipFreeAsync on `stream` after the call's kernels,
+ * so calls on different streams (or host threads) never share it and nothing
+ * is cached per stream.  The pool keeps up to 256 MiB of freed workspace
+ * across synchronisations for reuse; gt_workspace_release() returns it to
+ * the device.
  *
  * Semantics: asynchronous.  GT_SUCCESS means the work was enqueued on
  * `stream`; device faults surface at the caller's next synchronisation.
@@ -192,8 +195,8 @@ gt_status gt_gatv2_fwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* col
  * in `dtype` (bf16 rounded to nearest even); they must not overlap the
  * inputs or each other.  With bf16 features the two dot products per entry
  * are bf16 dot products accumulated in fp32, and each entry's coefficients
- * (ds and alpha) are rounded to bf16 before they multiply its vectors.  Asynchronous on `stream`; uses the stream's cached
- * workspace.
+ * (ds and alpha) are rounded to bf16 before they multiply its vectors.
+ * Asynchronous on `stream`; workspace as for gt_attn_fwd.
  */
 gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx,
                       const int64_t* rowptr_t, const int32_t* colidx_t, const void* Q,
@@ -283,8 +286,17 @@ gt_status gt_profile_enable(int32_t enable);
 gt_status gt_profile_collect(double ms[3], int64_t* calls);
 
 /*
- * Frees every cached workspace (synchronising each device that holds one).
- * Must not run concurrently with attention calls.
+ * Memory of the library's workspace pool on `device` (host outputs): bytes
+ * the pool holds from the device, and bytes of it in use by calls whose
+ * workspace is not yet freed in stream order.  Both 0 before the device's
+ * first call.
+ */
+gt_status gt_workspace_pool_stats(int32_t device, uint64_t* reserved_bytes, uint64_t* used_bytes);
+
+/*
+ * Returns the unused memory of the library's workspace pools to the devices
+ * (hipMemPoolTrimTo).  Workspace of calls still in flight is not affected;
+ * safe to call at any time from any thread.
  */
 gt_status gt_workspace_release(void);
 

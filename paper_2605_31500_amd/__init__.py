@@ -28,6 +28,7 @@ EXPORTED_SYMBOLS = (
     "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
     "gt_segment_reduce", "gt_dot_aggr", "gt_csr_validate", "gt_status_string",
     "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
+    "gt_workspace_pool_stats",
 )
 
 
@@ -76,9 +77,11 @@ def load_library(path: str = LIB_PATH):
     L.gt_profile_enable.argtypes = [i32]
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     L.gt_workspace_release.argtypes = []
+    L.gt_workspace_pool_stats.argtypes = [i32, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)]
     for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
                  "gt_segment_reduce", "gt_dot_aggr", "gt_csr_validate",
-                 "gt_profile_enable", "gt_profile_collect", "gt_workspace_release"):
+                 "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
+                 "gt_workspace_pool_stats"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -334,6 +337,15 @@ def gt_profile_collect():
     calls = ctypes.c_int64(0)
     _check(load_library().gt_profile_collect(ms, ctypes.byref(calls)))
     return [ms[0], ms[1], ms[2]], calls.value
+
+
+def gt_workspace_pool_stats(device=None):
+    """(reserved_bytes, used_bytes) of the library's workspace pool on a device
+    (default: the current one)."""
+    dev = torch.cuda.current_device() if device is None else int(device)
+    r, u = ctypes.c_uint64(0), ctypes.c_uint64(0)
+    _check(load_library().gt_workspace_pool_stats(dev, ctypes.byref(r), ctypes.byref(u)))
+    return r.value, u.value
 
 
 def gt_workspace_release() -> None:

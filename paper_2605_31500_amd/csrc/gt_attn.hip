@@ -58,12 +58,9 @@ constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kXcds = 8;
 
-// Counter slots in the workspace (reset to zero at the start of each call).
-// Work-list counters.  Each counter sits on its own 256-byte line so that
-// atomics on different counters do not serialise on one cache line.  A
-// workspace holds two counter sets used by alternate calls: a call uses one
-// set (zero on entry) and its attention kernel zeroes the other set for the
-// next call, so no reset has to wait for the end of the call.
+// Work-list counters in the workspace, cleared by a fill kernel at the start
+// of each call.  Each counter sits on its own 256-byte line so that atomics
+// on different counters do not serialise on one cache line.
 // Score kinds of the attention skeleton.
 enum { KIND_GT = 0, KIND_GATV2 = 1 };
 
@@ -125,7 +122,6 @@ struct AttnParams {
     int32_t light_max;
     int32_t cap_items;
     const int32_t* counters;
-    int32_t* next_counters;  // the other counter set, zeroed for the next call
     const int32_t* med_list;
     const ChunkItem* chunks;
     float* part_acc;   // [slot][H*D]
@@ -672,7 +668,6 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
 
     // Counts come from the partition kernel; clamping keeps every list read
     // inside the workspace even if the CSR precondition were violated.
-    if (blockIdx.x == 0 && threadIdx.x < CNT_COUNT) CNT(p.next_counters, threadIdx.x) = 0;
     const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_items);
     const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
     const int nwaves = gridDim.x * kWavesPerBlock;
@@ -1272,6 +1267,13 @@ __global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
     }
 }
 
+// Clears n ints (the work-list counters at the start of a call).  A kernel
+// rather than hipMemsetAsync, so that a call recorded into a HIP graph holds
+// no memset node.
+__global__ void __launch_bounds__(kBlock) gt_clear_kernel(int32_t* __restrict__ p, int32_t n) {
+    for (int32_t i = threadIdx.x; i < n; i += kBlock) p[i] = 0;
+}
+
 __global__ void __launch_bounds__(kBlock) gt_csr_check_kernel(const int64_t* rowptr, const int32_t* colidx,
                                                             int64_t N, int64_t E, int32_t* bad) {
     const int64_t stride = (int64_t)gridDim.x * kBlock;
@@ -1343,48 +1345,85 @@ struct PhaseEvents {
     }
 };
 
-// Workspace cache: one buffer per (device, stream) -- per thread for the
-// per-thread default stream -- reused by every later call on that stream, so
-// steady-state calls allocate nothing and stream order keeps reuse safe.  The
-// buffer grows (stream-ordered free + allocation) when a call needs more.  The
-// entry's mutex is held while a call enqueues its whole kernel sequence, so
-// calls from several host threads on one stream cannot interleave.
-struct WsKey {
-    int dev;
-    uintptr_t stream;
-    size_t thread;
-    bool operator<(const WsKey& o) const {
-        if (dev != o.dev) return dev < o.dev;
-        if (stream != o.stream) return stream < o.stream;
-        return thread < o.thread;
+// Workspace.  Every call takes its own workspace (degree-bin lists, partial
+// states of split rows, work-list counters) from the library's memory pool of
+// the device, allocated and freed stream-ordered on the call's stream
+// (hipMallocFromPoolAsync / hipFreeAsync): calls on different streams never
+// share memory, and nothing is keyed by stream or pointer.  The pool keeps up
+// to kPoolKeepBytes of freed memory across synchronisations for reuse, so a
+// steady sequence of calls does not go back to the device allocator;
+// gt_workspace_release() returns the rest.
+constexpr int kMaxDevices = 64;
+constexpr uint64_t kPoolKeepBytes = uint64_t(256) << 20;
+
+struct DevicePools {
+    std::once_flag once[kMaxDevices];
+    hipMemPool_t pool[kMaxDevices] = {};
+    hipError_t err[kMaxDevices] = {};
+    std::atomic<bool> ready[kMaxDevices] = {};  // pool[dev] / err[dev] are set
+};
+DevicePools& device_pools() {
+    static DevicePools* p = new DevicePools();
+    return *p;
+}
+
+hipError_t pool_of(int dev, hipMemPool_t* out) {
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    DevicePools& dp = device_pools();
+    std::call_once(dp.once[dev], [&] {
+        hipMemPoolProps props;
+        std::memset(&props, 0, sizeof props);
+        props.allocType = hipMemAllocationTypePinned;
+        props.handleTypes = hipMemHandleTypeNone;
+        props.location.type = hipMemLocationTypeDevice;
+        props.location.id = dev;
+        hipMemPool_t pool = nullptr;
+        hipError_t e = hipMemPoolCreate(&pool, &props);
+        if (e == hipSuccess) {
+            uint64_t keep = kPoolKeepBytes;
+            e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+        }
+        dp.pool[dev] = pool;
+        dp.err[dev] = e;
+        dp.ready[dev].store(true, std::memory_order_release);
+    });
+    *out = dp.pool[dev];
+    return dp.err[dev];
+}
+
+// One call's workspace; freed stream-ordered after the call's kernels when it
+// goes out of scope (also on an error return after some launches).
+struct CallWorkspace {
+    char* ptr = nullptr;
+    hipStream_t stream = nullptr;
+    bool pooled = false;
+    CallWorkspace() = default;
+    CallWorkspace(const CallWorkspace&) = delete;
+    CallWorkspace& operator=(const CallWorkspace&) = delete;
+    ~CallWorkspace() {
+        if (pooled && ptr) (void)hipFreeAsync(ptr, stream);
     }
 };
 
-struct WsEntry {
-    std::mutex mu;
-    char* ptr = nullptr;
-    size_t bytes = 0;
-    bool counters_zero = false;  // counter set `parity` known to be zero
-    int parity = 0;              // counter set the next call uses
-};
-
-struct WsCache {
-    std::mutex mu;
-    std::map<WsKey, std::unique_ptr<WsEntry>> entries;
-};
-WsCache& ws_cache() {
-    static WsCache* c = new WsCache();
-    return *c;
+gt_status acquire_workspace(int dev, size_t bytes, hipStream_t stream, CallWorkspace& ws) {
+    hipMemPool_t pool = nullptr;
+    hipError_t he = pool_of(dev, &pool);
+    if (he != hipSuccess) return hip_fail(he, "workspace pool");
+    ws.stream = stream;
+    he = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws.ptr), bytes, pool, stream);
+    if (he != hipSuccess || !ws.ptr) {
+        (void)hipGetLastError();
+        ws.ptr = nullptr;
+        return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
+    }
+    ws.pooled = true;
+    return GT_SUCCESS;
 }
 
-WsEntry& ws_entry(int dev, hipStream_t stream) {
-    WsKey key{dev, reinterpret_cast<uintptr_t>(stream), 0};
-    if (stream == hipStreamPerThread) key.thread = std::hash<std::thread::id>()(std::this_thread::get_id());
-    WsCache& c = ws_cache();
-    std::lock_guard<std::mutex> lk(c.mu);
-    auto& e = c.entries[key];
-    if (!e) e.reset(new WsEntry());
-    return *e;
+// Zeroes `n` counter ints of a fresh workspace, in stream order.
+hipError_t clear_counters(int32_t* p, int n, hipStream_t stream) {
+    hipLaunchKernelGGL(gt_clear_kernel, dim3(1), dim3(kBlock), 0, stream, p, n);
+    return hipGetLastError();
 }
 
 struct Args {
@@ -1523,7 +1562,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     // workspace: counters | medium rows | heavy rows | chunk items | partial (m,l) | partial acc
     const PartCaps caps = part_caps(a.E, heavy_min, chunk);
     size_t off = 0;
-    const size_t o_cnt = off;      off = align_up(off + 2 * kCntSetWords * sizeof(int32_t), 256);
+    const size_t o_cnt = off;      off = align_up(off + kCntSetWords * sizeof(int32_t), 256);
     const size_t o_med = off;      off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
     const size_t o_heavy = off;    off = align_up(off + (size_t)caps.heavy * sizeof(HeavyRow), 256);
     const size_t o_chunks = off;   off = align_up(off + (size_t)caps.items * sizeof(ChunkItem), 256);
@@ -1533,36 +1572,15 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     off = align_up(off + ((tiles || !SortedLight<T, H, D, KIND>::value) ? 0 : (size_t)a.N * sizeof(int32_t)), 256);
     const size_t ws_bytes = off;
 
-    WsEntry& we = ws_entry(dev, stream);
-    std::lock_guard<std::mutex> ws_lock(we.mu);
-    if (we.bytes < ws_bytes) {
-        if (we.ptr) (void)hipFreeAsync(we.ptr, stream);
-        we.ptr = nullptr;
-        we.bytes = 0;
-        he = hipMallocAsync(reinterpret_cast<void**>(&we.ptr), ws_bytes, stream);
-        if (he != hipSuccess || !we.ptr) {
-            (void)hipGetLastError();
-            we.ptr = nullptr;
-            return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(ws_bytes) + " bytes failed");
-        }
-        we.bytes = ws_bytes;
-        we.counters_zero = false;
-    }
-    char* ws = we.ptr;
-    int32_t* cnt_sets = reinterpret_cast<int32_t*>(ws + o_cnt);
-    if (!we.counters_zero) {
-        he = hipMemsetAsync(cnt_sets, 0, 2 * kCntSetWords * sizeof(int32_t), stream);
-        if (he != hipSuccess) return hip_fail(he, "hipMemsetAsync");
-        we.parity = 0;
-    }
-    int32_t* counters = cnt_sets + we.parity * kCntSetWords;
-    int32_t* next_counters = cnt_sets + (1 - we.parity) * kCntSetWords;
-    // Until the attention kernel (which zeroes the other set) is enqueued, the
-    // next call cannot rely on its counters; a failed launch leaves this false.
-    we.counters_zero = false;
+    CallWorkspace cw;
+    gt_status st = acquire_workspace(dev, ws_bytes, stream, cw);
+    if (st != GT_SUCCESS) return st;
+    char* ws = cw.ptr;
+    int32_t* counters = reinterpret_cast<int32_t*>(ws + o_cnt);
 
     PhaseEvents ph;
     if ((he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
+    if ((he = clear_counters(counters, kCntSetWords, stream)) != hipSuccess) return hip_fail(he, "counter clear");
 
     PartParams pp;
     pp.rowptr = a.rowptr;
@@ -1616,7 +1634,6 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.light_max = light_max;
     ap.cap_items = (int32_t)caps.items;
     ap.counters = counters;
-    ap.next_counters = next_counters;
     ap.med_list = pp.med_list;
     ap.chunks = pp.chunks;
     ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
@@ -1642,8 +1659,6 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     hipLaunchKernelGGL((gt_merge_kernel<T, H, D>), dim3(merge_grid), dim3(kBlock), 0, stream, mp);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "merge launch");
     ph.commit(stream);
-    we.parity = 1 - we.parity;
-    we.counters_zero = true;
     return GT_SUCCESS;
 }
 
@@ -1939,25 +1954,36 @@ gt_status gt_profile_collect(double ms[3], int64_t* calls) {
     return st;
 }
 
+gt_status gt_workspace_pool_stats(int32_t device, uint64_t* reserved_bytes, uint64_t* used_bytes) {
+    t_last_error.clear();
+    if (!reserved_bytes || !used_bytes) return fail(GT_ERROR_INVALID_VALUE, "null output");
+    *reserved_bytes = 0;
+    *used_bytes = 0;
+    if (device < 0 || device >= kMaxDevices) return fail(GT_ERROR_INVALID_VALUE, "device out of range");
+    DevicePools& dp = device_pools();
+    if (!dp.ready[device].load(std::memory_order_acquire) || !dp.pool[device]) return GT_SUCCESS;
+    uint64_t r = 0, u = 0;
+    hipError_t he = hipMemPoolGetAttribute(dp.pool[device], hipMemPoolAttrReservedMemCurrent, &r);
+    if (he == hipSuccess) he = hipMemPoolGetAttribute(dp.pool[device], hipMemPoolAttrUsedMemCurrent, &u);
+    if (he != hipSuccess) return hip_fail(he, "hipMemPoolGetAttribute");
+    *reserved_bytes = r;
+    *used_bytes = u;
+    return GT_SUCCESS;
+}
+
 gt_status gt_workspace_release(void) {
     t_last_error.clear();
-    WsCache& c = ws_cache();
-    std::lock_guard<std::mutex> lk(c.mu);
-    int cur = 0;
-    (void)hipGetDevice(&cur);
+    DevicePools& dp = device_pools();
     gt_status st = GT_SUCCESS;
-    for (auto& kv : c.entries) {
-        std::lock_guard<std::mutex> el(kv.second->mu);
-        if (!kv.second->ptr) continue;
-        hipError_t he = hipSetDevice(kv.first.dev);
-        if (he == hipSuccess) he = hipDeviceSynchronize();
-        if (he == hipSuccess) he = hipFree(kv.second->ptr);
-        if (he != hipSuccess) st = hip_fail(he, "releasing a workspace");
-        kv.second->ptr = nullptr;
-        kv.second->bytes = 0;
+    for (int dev = 0; dev < kMaxDevices; ++dev) {
+        // a device's pool is created by its first call; devices without one
+        // are skipped
+        if (!dp.ready[dev].load(std::memory_order_acquire)) continue;
+        hipMemPool_t pool = dp.pool[dev];
+        if (!pool) continue;
+        const hipError_t he = hipMemPoolTrimTo(pool, 0);
+        if (he != hipSuccess) st = hip_fail(he, "trimming a workspace pool");
     }
-    c.entries.clear();
-    (void)hipSetDevice(cur);
     return st;
 }
 

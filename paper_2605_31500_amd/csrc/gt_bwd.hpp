@@ -41,7 +41,6 @@ struct BwdParams {
     int32_t cap_items;
     int32_t cap_heavy;
     const int32_t* counters;
-    int32_t* next_counters;
     const int32_t* med_list;
     const ChunkItem* chunks;
     const HeavyRow* heavy;
@@ -271,7 +270,6 @@ __global__ void __launch_bounds__(kBlock) gt_bwd_kernel(BwdParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
     int32_t* tile = tiles[wv];
-    if (blockIdx.x == 0 && threadIdx.x < CNT_COUNT) CNT(p.next_counters, threadIdx.x) = 0;
     const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_items);
     const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
     const int nwaves = gridDim.x * kWavesPerBlock;
@@ -414,33 +412,15 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
     const size_t o_delta = off;  off = align_up(off + (size_t)a.N * H * sizeof(float), 256);
     const size_t ws_bytes = off;
 
-    WsEntry& we = ws_entry(dev, stream);
-    std::lock_guard<std::mutex> ws_lock(we.mu);
-    if (we.bytes < ws_bytes) {
-        if (we.ptr) (void)hipFreeAsync(we.ptr, stream);
-        we.ptr = nullptr;
-        we.bytes = 0;
-        he = hipMallocAsync(reinterpret_cast<void**>(&we.ptr), ws_bytes, stream);
-        if (he != hipSuccess || !we.ptr) {
-            (void)hipGetLastError();
-            we.ptr = nullptr;
-            return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(ws_bytes) + " bytes failed");
-        }
-        we.bytes = ws_bytes;
-        we.counters_zero = false;
-    }
-    char* ws = we.ptr;
-    int32_t* cnt_sets = reinterpret_cast<int32_t*>(ws + o_cnt);
-    if (!we.counters_zero) {
-        he = hipMemsetAsync(cnt_sets, 0, 2 * kCntSetWords * sizeof(int32_t), stream);
-        if (he != hipSuccess) return hip_fail(he, "hipMemsetAsync");
-        we.parity = 0;
-    }
-    we.counters_zero = false;
+    CallWorkspace cw;
+    gt_status st = acquire_workspace(dev, ws_bytes, stream, cw);
+    if (st != GT_SUCCESS) return st;
+    char* ws = cw.ptr;
+    int32_t* cnt_sets = reinterpret_cast<int32_t*>(ws + o_cnt);  // one counter set per pass
+    if ((he = clear_counters(cnt_sets, 2 * kCntSetWords, stream)) != hipSuccess) return hip_fail(he, "counter clear");
 
     for (int mode = 0; mode < 2; ++mode) {
-        int32_t* counters = cnt_sets + we.parity * kCntSetWords;
-        int32_t* next_counters = cnt_sets + (1 - we.parity) * kCntSetWords;
+        int32_t* counters = cnt_sets + mode * kCntSetWords;
         const int64_t* rp = mode == 0 ? a.rowptr : a.rowptr_t;
         const int32_t* ci = mode == 0 ? a.colidx : a.colidx_t;
 
@@ -478,7 +458,6 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
         bp.cap_items = (int32_t)caps.items;
         bp.cap_heavy = (int32_t)caps.heavy;
         bp.counters = counters;
-        bp.next_counters = next_counters;
         bp.med_list = pp.med_list;
         bp.chunks = pp.chunks;
         bp.heavy = pp.heavy;
@@ -496,9 +475,7 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
             hipLaunchKernelGGL((gt_bwd_merge_kernel<T, H, D, 1>), dim3(merge_grid), dim3(kBlock), 0, stream, bp);
         }
         if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "backward merge launch");
-        we.parity = 1 - we.parity;
     }
-    we.counters_zero = true;
     return GT_SUCCESS;
 }
 

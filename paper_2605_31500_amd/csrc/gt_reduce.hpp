@@ -46,7 +46,6 @@ struct ReduceParams {
     int32_t cap_items;
     int32_t cap_heavy;
     const int32_t* counters;
-    int32_t* next_counters;
     const int32_t* med_list;
     const ChunkItem* chunks;
     const HeavyRow* heavy;
@@ -279,7 +278,6 @@ __global__ void __launch_bounds__(kBlock) gt_reduce_kernel(ReduceParams p) {
     const int wv = threadIdx.x / kWave;
     int32_t* tile = tiles[wv];
 
-    if (blockIdx.x == 0 && threadIdx.x < CNT_COUNT) CNT(p.next_counters, threadIdx.x) = 0;
     const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_items);
     const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
     const int nwaves = gridDim.x * kWavesPerBlock;
@@ -402,41 +400,22 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     // workspace: counters | medium rows | split rows | chunk items | partials
     const PartCaps caps = part_caps(a.E, heavy_min, chunk);
     size_t off = 0;
-    const size_t o_cnt = off;    off = align_up(off + 2 * kCntSetWords * sizeof(int32_t), 256);
+    const size_t o_cnt = off;    off = align_up(off + kCntSetWords * sizeof(int32_t), 256);
     const size_t o_med = off;    off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
     const size_t o_heavy = off;  off = align_up(off + (size_t)caps.heavy * sizeof(HeavyRow), 256);
     const size_t o_chunks = off; off = align_up(off + (size_t)caps.items * sizeof(ChunkItem), 256);
     const size_t o_part = off;   off = align_up(off + (size_t)caps.slots * Gm::kF * sizeof(uint64_t), 256);
     const size_t ws_bytes = off;
 
-    WsEntry& we = ws_entry(dev, stream);
-    std::lock_guard<std::mutex> ws_lock(we.mu);
-    if (we.bytes < ws_bytes) {
-        if (we.ptr) (void)hipFreeAsync(we.ptr, stream);
-        we.ptr = nullptr;
-        we.bytes = 0;
-        he = hipMallocAsync(reinterpret_cast<void**>(&we.ptr), ws_bytes, stream);
-        if (he != hipSuccess || !we.ptr) {
-            (void)hipGetLastError();
-            we.ptr = nullptr;
-            return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(ws_bytes) + " bytes failed");
-        }
-        we.bytes = ws_bytes;
-        we.counters_zero = false;
-    }
-    char* ws = we.ptr;
-    int32_t* cnt_sets = reinterpret_cast<int32_t*>(ws + o_cnt);
-    if (!we.counters_zero) {
-        he = hipMemsetAsync(cnt_sets, 0, 2 * kCntSetWords * sizeof(int32_t), stream);
-        if (he != hipSuccess) return hip_fail(he, "hipMemsetAsync");
-        we.parity = 0;
-    }
-    int32_t* counters = cnt_sets + we.parity * kCntSetWords;
-    int32_t* next_counters = cnt_sets + (1 - we.parity) * kCntSetWords;
-    we.counters_zero = false;
+    CallWorkspace cw;
+    gt_status st = acquire_workspace(dev, ws_bytes, stream, cw);
+    if (st != GT_SUCCESS) return st;
+    char* ws = cw.ptr;
+    int32_t* counters = reinterpret_cast<int32_t*>(ws + o_cnt);
 
     PhaseEvents ph;
     if ((he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
+    if ((he = clear_counters(counters, kCntSetWords, stream)) != hipSuccess) return hip_fail(he, "counter clear");
 
     PartParams pp;
     pp.rowptr = a.rowptr;
@@ -467,7 +446,6 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     rp.cap_items = (int32_t)caps.items;
     rp.cap_heavy = (int32_t)caps.heavy;
     rp.counters = counters;
-    rp.next_counters = next_counters;
     rp.med_list = pp.med_list;
     rp.chunks = pp.chunks;
     rp.heavy = pp.heavy;
@@ -481,8 +459,6 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     hipLaunchKernelGGL((gt_reduce_merge_kernel<T, NVEC>), dim3(merge_grid), dim3(kBlock), 0, stream, rp);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "reduce merge launch");
     ph.commit(stream);
-    we.parity = 1 - we.parity;
-    we.counters_zero = true;
     return GT_SUCCESS;
 }
 

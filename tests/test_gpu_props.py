@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import synth
-from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, run_gpu, sample_rows,
+from tests.helpers import (TOL_BF16, TOL_F32, bf16_bits_to_f32, gate_error, run_gpu, sample_rows, workload,
                            score_rounding_bound, to_device, to_host_f32)
 
 pytestmark = pytest.mark.gpu
@@ -103,8 +103,8 @@ def test_non_default_stream():
 
 
 def test_concurrent_host_threads_and_streams():
-    """Four host threads, each with its own stream (and so its own cached
-    workspace), issue interleaved calls on different graphs and settings; every
+    """Four host threads, each with its own stream, issue interleaved calls on
+    different graphs and settings (every call has its own workspace); every
     result equals the same call made alone."""
     import threading
     import paper_2605_31500_amd as gtm
@@ -184,7 +184,7 @@ def test_degree_agnostic_mappings(mode):
     function: parity on the power-law workload, whose hub rows then run whole
     on one group or one wave."""
     import bench
-    w = synth.config(1)
+    w = workload(1)
     got = run_gpu(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, tuning=bench.ABLATION_MODES[mode])
     ref, absagg, _ = oracle.gt_attn_fwd(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, want_lse=False)
     assert gate_error(got, ref, absagg) <= TOL_F32
@@ -336,8 +336,9 @@ def test_profiler_counts_calls():
 
 
 def test_workspace_reuse_growth_and_release():
-    """Consecutive calls share the per-stream workspace; its counters must be
-    back at zero after every call and growth must not disturb results."""
+    """Consecutive calls of different sizes reuse pooled workspace memory; the
+    counters of every call start at zero and results do not depend on what a
+    workspace held before."""
     small = synth.ragged_graph(11, 3000, max_deg=30, hubs={1: 2999, 2: 1500})
     big = synth.ragged_graph(12, 40000, max_deg=50, hubs={5: 39999, 6: 20000, 7: 5000})
     feats = {n: synth.features(13, n, 4, 32, "f32") for n in (3000, 40000)}
@@ -395,13 +396,13 @@ def test_step_ordered_light_rows(dtype, tuning):
 def test_small_graph_short_chunks(kind, N):
     """Small power-law graphs take short chunks for their hub rows (a few
     hundred entries; on 16K nodes the largest hub is cut into the full 32
-    chunks): the hubs and a sample of other rows match the oracle under the
-    default partition."""
+    chunks): the hubs and all other rows match the oracle under the
+    default partition (every row)."""
     import paper_2605_31500_amd as m
     H, D = 4, 32
     rowptr, colidx = synth.chung_lu_graph(0, N)
     Q, K, V = synth.features(0, N, H, D, "f32")
-    rows = sample_rows(rowptr, 200, 40, seed=N)
+    rows = np.arange(N, dtype=np.int64)
     assert np.diff(rowptr).max() > 32 * 192  # the largest hub has more entries than 32 short chunks hold
     dt = [to_device(x) for x in (rowptr, colidx, Q, K)]
     out = torch.empty_like(dt[2])
@@ -415,3 +416,53 @@ def test_small_graph_short_chunks(kind, N):
     torch.cuda.synchronize()
     got = to_host_f32(out)[rows]
     assert gate_error(got, ref, absagg) <= TOL_F32
+
+
+def test_workspace_memory_comes_back_after_many_streams():
+    """Calls on 50 streams created and dropped one after another: workspace is
+    per call (pooled, stream-ordered), so the memory the library's pool holds
+    afterwards is bounded by its 256 MiB reuse threshold, not 50 workspaces;
+    none of it is in use once the calls are done, and gt_workspace_release()
+    returns all of it to the device.  Each call's workspace here is about
+    40 MB (short chunks give many partial states)."""
+    import paper_2605_31500_amd as gtm
+    N, H, D = 200_000, 4, 32
+    rowptr, colidx = synth.chung_lu_graph(3, N)
+    Q, K, V = synth.features(3, N, H, D, "f32")
+    dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    out = torch.empty_like(dev[2])
+    tuning = {"light_max_deg": 2, "heavy_min_deg": 3, "chunk_edges": 64, "grid_blocks": 0}
+    gtm.gt_attn_fwd_ex(*dev, out, np.float32(0.2), tuning=tuning)
+    torch.cuda.synchronize()
+    want = to_host_f32(out)
+    # streams themselves hold some device memory in the runtime; create and
+    # drop 50 first, so that the measurement below sees only the workspace
+    for _ in range(50):
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            torch.zeros(1, device="cuda")
+        s.synchronize()
+        del s
+    gtm.gt_workspace_release()
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info()[0]
+    assert gtm.gt_workspace_pool_stats() == (0, 0)
+    for _ in range(50):
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            gtm.gt_attn_fwd_ex(*dev, out, np.float32(0.2), tuning=tuning, stream=s)
+        s.synchronize()
+        del s
+    torch.cuda.synchronize()
+    reserved, used = gtm.gt_workspace_pool_stats()
+    print("pool after 50 streams: reserved %d MiB, used %d MiB" % (reserved >> 20, used >> 20), flush=True)
+    assert used == 0 and 0 < reserved <= (256 << 20) + (64 << 20)
+    held = free0 - torch.cuda.mem_get_info()[0]
+    assert held <= (256 << 20) + (64 << 20), "held %d MiB after 50 streams" % (held >> 20)
+    assert np.array_equal(to_host_f32(out), want)
+    gtm.gt_workspace_release()
+    torch.cuda.synchronize()
+    assert gtm.gt_workspace_pool_stats() == (0, 0)
+    back = free0 - torch.cuda.mem_get_info()[0]
+    print("device memory not returned: %d MiB" % (back >> 20), flush=True)
+    assert back <= (8 << 20), "%d MiB not returned" % (back >> 20)
