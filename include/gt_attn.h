@@ -155,6 +155,26 @@ gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* c
                          const gt_tuning* tuning, hipStream_t stream);
 
 /*
+ * Allocation-free variant of gt_attn_fwd_ex, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation.  Same arguments, results (bit-identical to
+ * gt_attn_fwd_ex with the same settings), validation and asynchrony; it calls
+ * no hipMalloc, hipFree or other allocating routine, and records no
+ * profiling events.  Its workspace is a 256 MiB device array of the library
+ * (one per device, held from the library's load until the process ends):
+ * a call whose workspace would exceed it (very large graphs, or tunings with
+ * many short chunks) returns GT_ERROR_INVALID_VALUE and enqueues nothing.
+ * All calls of this entry point on one device share that array, and each
+ * call leaves its contents behind: calls that overlap in time on one device
+ * (concurrent streams, or host threads) race and give undefined results, so
+ * serialise them (one stream, or events between streams).
+ */
+gt_status gt_attn_fwd_noalloc(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx,
+                              const void* Q, const void* K, const void* V, void* out, float* lse,
+                              int64_t N, int64_t E, int32_t H, int32_t D, float scale,
+                              const gt_tuning* tuning, hipStream_t stream);
+
+/*
  * GATv2 forward (paper Section 2.2, the GATv2 member of the attention family;
  * Appendix D.2, "Fused forward in CSR (GATv2)"), on the same fused streaming
  * pass and degree-aware partition as gt_attn_fwd_ex:

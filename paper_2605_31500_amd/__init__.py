@@ -25,7 +25,7 @@ GT_DTYPE_F32 = 0
 GT_DTYPE_BF16 = 1
 
 EXPORTED_SYMBOLS = (
-    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
+    "gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_attn_fwd_noalloc", "gt_gatv2_fwd", "gt_attn_bwd",
     "gt_segment_reduce", "gt_dot_aggr", "gt_csr_validate", "gt_status_string",
     "gt_last_error_message", "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
     "gt_workspace_pool_stats",
@@ -62,6 +62,7 @@ def load_library(path: str = LIB_PATH):
     L.gt_attn_fwd.argtypes = sig
     L.gt_attn_fwd_bf16.argtypes = sig
     L.gt_attn_fwd_ex.argtypes = [ctypes.c_int] + sig[:6] + [P] + sig[6:-1] + [ctypes.POINTER(GtTuning), P]
+    L.gt_attn_fwd_noalloc.argtypes = L.gt_attn_fwd_ex.argtypes
     L.gt_gatv2_fwd.argtypes = [ctypes.c_int, P, P, P, P, P, f32, P, P, i64, i64, i32, i32,
                                ctypes.POINTER(GtTuning), P]
     L.gt_segment_reduce.argtypes = [ctypes.c_int, ctypes.c_int, P, P, P, P, P, i64, i64, i32,
@@ -78,7 +79,8 @@ def load_library(path: str = LIB_PATH):
     L.gt_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     L.gt_workspace_release.argtypes = []
     L.gt_workspace_pool_stats.argtypes = [i32, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)]
-    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_gatv2_fwd", "gt_attn_bwd",
+    for name in ("gt_attn_fwd", "gt_attn_fwd_bf16", "gt_attn_fwd_ex", "gt_attn_fwd_noalloc", "gt_gatv2_fwd",
+                 "gt_attn_bwd",
                  "gt_segment_reduce", "gt_dot_aggr", "gt_csr_validate",
                  "gt_profile_enable", "gt_profile_collect", "gt_workspace_release",
                  "gt_workspace_pool_stats"):
@@ -168,6 +170,28 @@ def gt_attn_fwd_ex(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None
     _check(load_library().gt_attn_fwd_ex(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
                                          _ptr(V), _ptr(out), _ptr(lse), N, colidx.numel(), H, D,
                                          float(scale), tp, _stream(Q.device, stream)))
+
+
+def gt_attn_fwd_noalloc(rowptr, colidx, Q, K, V, out, scale, tuning=None, stream=None, lse=None) -> None:
+    """As gt_attn_fwd_ex, through the allocation-free entry point (workspace in
+    the library's 256 MiB per-device scratch array; overlapping calls on one
+    device race)."""
+    if Q.dtype == torch.float32:
+        dtype, allowed = GT_DTYPE_F32, (torch.float32,)
+    else:
+        dtype, allowed = GT_DTYPE_BF16, (torch.bfloat16, torch.int16, torch.uint16)
+    _check_tensors(rowptr, colidx, Q, K, V, out, allowed)
+    N, H, D = Q.shape
+    if isinstance(tuning, dict):
+        tuning = GtTuning(**tuning)
+    tp = ctypes.byref(tuning) if tuning is not None else None
+    if lse is not None:
+        if not (lse.is_cuda and lse.device == out.device and lse.is_contiguous()
+                and lse.dtype == torch.float32 and tuple(lse.shape) == (N, H)):
+            raise ValueError("lse must be a contiguous float32 [N, H] device tensor")
+    _check(load_library().gt_attn_fwd_noalloc(dtype, _ptr(rowptr), _ptr(colidx), _ptr(Q), _ptr(K),
+                                              _ptr(V), _ptr(out), _ptr(lse), N, colidx.numel(), H, D,
+                                              float(scale), tp, _stream(Q.device, stream)))
 
 
 def gt_gatv2_fwd(rowptr, colidx, L, R, att, slope, out, tuning=None, stream=None, lse=None) -> None:

@@ -51,6 +51,14 @@
 
 #include "gt_attn.h"
 
+// Workspace of the allocation-free entry point (gt_attn_fwd_noalloc): one
+// array per device, held from the library's load until the process ends.
+// Host code never passes `scratch` itself to a kernel (in host code the name
+// is a stand-in, not a device address): it takes the device address from
+// hipGetSymbolAddress once per device (scratch_of below).
+constexpr size_t kScratchBytes = size_t(256) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
 namespace {
 
 constexpr int kWave = 64;
@@ -1420,6 +1428,48 @@ gt_status acquire_workspace(int dev, size_t bytes, hipStream_t stream, CallWorks
     return GT_SUCCESS;
 }
 
+// Device address of the scratch array on device `dev` (the current device),
+// looked up once per device.
+struct ScratchAddrs {
+    std::once_flag once[kMaxDevices];
+    char* ptr[kMaxDevices] = {};
+    hipError_t err[kMaxDevices] = {};
+};
+ScratchAddrs& scratch_addrs() {
+    static ScratchAddrs* s = new ScratchAddrs();
+    return *s;
+}
+
+hipError_t scratch_of(int dev, char** out) {
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    ScratchAddrs& sa = scratch_addrs();
+    std::call_once(sa.once[dev], [&] {
+        void* p = nullptr;
+        sa.err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        sa.ptr[dev] = sa.err[dev] == hipSuccess ? static_cast<char*>(p) : nullptr;
+    });
+    *out = sa.ptr[dev];
+    if (sa.err[dev] == hipSuccess && !sa.ptr[dev]) return hipErrorInvalidSymbol;
+    return sa.err[dev];
+}
+
+// The workspace of one call: from the pool, or (allocation-free entry point)
+// the device's scratch array, whose size bounds the accepted problems.
+gt_status call_workspace(bool noalloc, int dev, size_t bytes, hipStream_t stream, CallWorkspace& ws) {
+    if (!noalloc) return acquire_workspace(dev, bytes, stream, ws);
+    if (bytes > kScratchBytes)
+        return fail(GT_ERROR_INVALID_VALUE, "the call needs " + std::to_string(bytes) +
+                                                " bytes of workspace, more than the " + std::to_string(kScratchBytes) +
+                                                "-byte scratch array of gt_attn_fwd_noalloc");
+    char* p = nullptr;
+    const hipError_t he = scratch_of(dev, &p);
+    if (he != hipSuccess) return hip_fail(he, "hipGetSymbolAddress(scratch)");
+    ws.ptr = p;
+    ws.stream = stream;
+    ws.pooled = false;
+    return GT_SUCCESS;
+}
+
 // Zeroes `n` counter ints of a fresh workspace, in stream order.
 hipError_t clear_counters(int32_t* p, int n, hipStream_t stream) {
     hipLaunchKernelGGL(gt_clear_kernel, dim3(1), dim3(kBlock), 0, stream, p, n);
@@ -1440,6 +1490,7 @@ struct Args {
     int kind = KIND_GT;
     const float* att = nullptr;  // GATv2 attention vector
     float slope = 0.0f;          // GATv2 LeakyReLU slope
+    bool noalloc = false;        // workspace from the scratch array, no allocation
 };
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -1573,13 +1624,15 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const size_t ws_bytes = off;
 
     CallWorkspace cw;
-    gt_status st = acquire_workspace(dev, ws_bytes, stream, cw);
+    gt_status st = call_workspace(a.noalloc, dev, ws_bytes, stream, cw);
     if (st != GT_SUCCESS) return st;
     char* ws = cw.ptr;
     int32_t* counters = reinterpret_cast<int32_t*>(ws + o_cnt);
 
+    // (the allocation-free entry point records no profiling events: creating
+    // them is a runtime allocation)
     PhaseEvents ph;
-    if ((he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
+    if (!a.noalloc && (he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
     if ((he = clear_counters(counters, kCntSetWords, stream)) != hipSuccess) return hip_fail(he, "counter clear");
 
     PartParams pp;
@@ -1841,6 +1894,14 @@ gt_status gt_attn_fwd_ex(gt_dtype dtype, const int64_t* rowptr, const int32_t* c
                          const void* K, const void* V, void* out, float* lse, int64_t N, int64_t E, int32_t H,
                          int32_t D, float scale, const gt_tuning* tuning, hipStream_t stream) {
     return run(dtype, Args{rowptr, colidx, Q, K, V, out, lse, N, E, H, D, scale}, tuning, stream);
+}
+
+gt_status gt_attn_fwd_noalloc(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const void* Q,
+                              const void* K, const void* V, void* out, float* lse, int64_t N, int64_t E, int32_t H,
+                              int32_t D, float scale, const gt_tuning* tuning, hipStream_t stream) {
+    Args a{rowptr, colidx, Q, K, V, out, lse, N, E, H, D, scale};
+    a.noalloc = true;
+    return run(dtype, a, tuning, stream);
 }
 
 gt_status gt_gatv2_fwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* colidx, const void* L, const void* R,
