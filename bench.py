@@ -335,6 +335,15 @@ def run_size_sweep(args, gt, torch, to_device, synth) -> int:
     return 0
 
 
+def pv_weights(w, args) -> str:
+    """How a bf16 line multiplies softmax weights with value rows."""
+    if args.gatv2:
+        return "fp32 weights x widened value rows"
+    if args.weights_fp32:
+        return "fp32 weights x widened value rows (dense tiles: two bf16 terms per weight)"
+    return "weights rounded to bf16 before P*V (fp32 accumulation; normaliser from fp32 weights)"
+
+
 def gatv2_attention_vector(w, seed: int):
     import math
     import synth
@@ -603,8 +612,11 @@ def main() -> int:
                     help="feature dtype of --hd-sweep (default f32)")
     ap.add_argument("--study-features", default="32,128,512", help="feature widths of the study")
     ap.add_argument("--dense-tiles", type=int, default=0, metavar="MIN",
-                    help="enable the matrix-core path for dense 64-id windows holding at "
-                         "least MIN in-window entries (bf16, H*D <= 128)")
+                    help="threshold of the matrix-core path for dense 64-id windows (bf16, "
+                         "H*D <= 128): windows estimated to hold at least MIN in-window entries; "
+                         "0 = the library default (256), -1 = off")
+    ap.add_argument("--weights-fp32", action="store_true",
+                    help="bf16 features: keep the softmax weights in fp32 for P*V (gt_tuning.weights_fp32)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run plain device-to-device copies of MIB "
                          "MiB (reference kernel for scaling HBM byte counters)")
@@ -644,7 +656,12 @@ def main() -> int:
     out = torch.empty_like(dev[2])
     stream = torch.cuda.current_stream()
 
-    tuning = {"dense_tiles": args.dense_tiles} if args.dense_tiles else None
+    tuning = {}
+    if args.dense_tiles:
+        tuning["dense_tiles"] = args.dense_tiles
+    if args.weights_fp32:
+        tuning["weights_fp32"] = 1
+    tuning = tuning or None
     att = gatv2_attention_vector(w, args.config) if args.gatv2 else None
     if args.gatv2:
         att_d = to_device(att)
@@ -690,11 +707,14 @@ def main() -> int:
     achieved = mbytes / (attn_ms * 1e-3) / 1e9
     key = w.name + (":gatv2" if args.gatv2 else "")
     traffic = stored_traffic(key)
+    # the dense-tile kernel runs (before the CSR kernel, in the timed
+    # attention phase) for bf16 graph-transformer rows of H*D <= 128
+    tile_path = (not args.gatv2 and w.dtype == "bf16" and w.H * w.D <= 128 and args.dense_tiles >= 0)
     got = gt.to_numpy_f32(out) if not args.no_cpu_baseline else None
 
     roofline = {
         "bound": "hbm",
-        "kernel": ("gt_tile_kernel + gt_attn_kernel" if args.dense_tiles else "gt_attn_kernel")
+        "kernel": ("gt_tile_kernel + gt_attn_kernel" if tile_path else "gt_attn_kernel")
                   + (" (GATv2 score)" if args.gatv2 else ""),
         "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBPS,
@@ -731,7 +751,8 @@ def main() -> int:
         "dtype": w.dtype,
         "data": "synthetic",
         "config": dict(w.describe(), **({"dense_tiles": args.dense_tiles} if args.dense_tiles else {}),
-                       **({"layer": "gatv2", "slope": GATV2_SLOPE} if args.gatv2 else {})),
+                       **({"layer": "gatv2", "slope": GATV2_SLOPE} if args.gatv2 else {}),
+                       **({"pv_weights": pv_weights(w, args)} if w.dtype == "bf16" else {})),
         "roofline": roofline,
         "phases_ms": {"partition": round(phase_ms[0] / calls, 5), "attention": round(attn_ms, 5),
                       "merge": round(phase_ms[2] / calls, 5)},

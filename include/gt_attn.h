@@ -111,24 +111,42 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  *                   between get one wavefront each (default 256)
  *   chunk_edges   : CSR entries per chunk of a split row, rounded up to a
  *                   multiple of 64; a row is cut into at most 32 chunks, so
- *                   very long rows get longer chunks (default 1024 on large
- *                   graphs; on small graphs shorter, down to 64, so that one
+ *                   very long rows get longer chunks (default: 1024 on large
+ *                   graphs, shorter on small ones, down to 64, so that one
  *                   chunk's chain of dependent steps stays within about half
- *                   the call's gather time)
+ *                   the call's gather time; the graph size where 1024 is
+ *                   reached depends on the bytes gathered per entry: the
+ *                   graph-transformer forward on the arxiv-shaped 169K-node
+ *                   fp32 4x32 graph gets 1024, the GATv2 forward 768)
  *   grid_blocks   : workgroups of the attention kernel, rounded up to a
  *                   multiple of 8 (default: about two light work items per
  *                   wavefront, within 4x..64x the resident workgroups)
- *   dense_tiles   : 0 (default) = off.  A positive value enables the matrix-
- *                   core path for locally dense graphs (Section 3.3 and
- *                   Appendix D.3: block-sparse tiles): rows are grouped in
- *                   aligned windows of 64 ids; a window whose light rows hold
- *                   at least `dense_tiles` entries pointing inside the window
- *                   computes those entries as masked 64x64 tiles with bf16
- *                   MFMA (scores and P*V), then streams each row's remaining
- *                   entries.  bf16 features with H*D <= 128 only; ignored
- *                   otherwise.  Softmax weights inside tiles are rounded to
- *                   bf16 before the P*V product (the normaliser uses the same
- *                   rounded weights).  256 suits 50%-dense 64-blocks.
+ *   dense_tiles   : threshold of the matrix-core path for locally dense
+ *                   graphs (Section 3.3 and Appendix D.3: block-sparse
+ *                   tiles); bf16 features with H*D <= 128 only, ignored
+ *                   otherwise.  0 (default) selects 256; a negative value
+ *                   turns the path off.  Rows are grouped in aligned windows
+ *                   of 64 ids.  The partition estimates each window's
+ *                   entries that point inside the window from a sample (the
+ *                   middle entry of every 8th light row) and lists the
+ *                   windows estimated to hold at least `dense_tiles` of them
+ *                   (with 1: every window with a light row).  The light rows
+ *                   of a listed window are computed by the tile kernel: their
+ *                   in-window entries as masked 64x64 tiles with bf16 MFMA
+ *                   (scores and P*V), then each row's remaining entries
+ *                   streamed; all other rows by the CSR kernel.  Softmax
+ *                   weights inside tiles are rounded to bf16 before the P*V
+ *                   product, as in the CSR step of bf16 rows; the normaliser
+ *                   and lse sum the fp32 weights.
+ *   weights_fp32  : bf16 features only (ignored for fp32).  0 (default):
+ *                   each softmax weight is rounded to bf16 before it
+ *                   multiplies its value row (P*V in bf16 products, fp32
+ *                   accumulation; out is then within 2^-8 sum_e alpha_e |v_e|
+ *                   of the fp32-weight result).  Nonzero: the weights stay
+ *                   fp32 and multiply the exactly widened value rows in fp32
+ *                   (in dense tiles: each weight as the sum of two bf16 terms,
+ *                   exact to 2^-17 relative, with two P*V products).
+ * Fields above 2^31 - 2^16 are refused (GT_ERROR_INVALID_VALUE).
  * Results are bitwise reproducible for fixed settings; different settings
  * change only the rounding.
  */
@@ -138,6 +156,7 @@ typedef struct gt_tuning {
     int32_t chunk_edges;
     int32_t grid_blocks;
     int32_t dense_tiles;
+    int32_t weights_fp32;
 } gt_tuning;
 
 /*

@@ -37,6 +37,7 @@
 
 #include <array>
 #include <atomic>
+#include <climits>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -70,9 +71,16 @@ constexpr int kXcds = 8;
 // of each call.  Each counter sits on its own 256-byte line so that atomics
 // on different counters do not serialise on one cache line.
 // Score kinds of the attention skeleton.
-enum { KIND_GT = 0, KIND_GATV2 = 1 };
+// KIND_GT_WF32: the graph-transformer score with the softmax weights kept in
+// fp32 for P*V (bf16 rows widen their value rows instead of pairing entries).
+enum { KIND_GT = 0, KIND_GATV2 = 1, KIND_GT_WF32 = 2 };
 
-enum { CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_SLOTS = 4, CNT_COUNT = 5 };
+// CNT_LIGHT: light rows left in the light-row order (shapes that build one);
+// CNT_WIN: dense-tile windows flagged by the partition.
+enum {
+    CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_SLOTS = 4, CNT_LIGHT = 5, CNT_WIN = 6,
+    CNT_COUNT = 7
+};
 constexpr int kCntStride = 64;                          // ints between counters
 constexpr int kCntSetWords = CNT_COUNT * kCntStride;   // one counter set
 #define CNT(c, i) ((c)[(i) * kCntStride])
@@ -134,7 +142,6 @@ struct AttnParams {
     const ChunkItem* chunks;
     float* part_acc;   // [slot][H*D]
     float2* part_ml;   // [slot][H]: (running max in log2 units, sum)
-    int32_t skip_light;  // light rows are handled by the dense-tile kernel
     const int32_t* light_list;  // [N]: light rows in step order per partition block, -1 elsewhere
 };
 
@@ -153,6 +160,13 @@ struct PartParams {
     ChunkItem* chunks;
     int32_t* light_list = nullptr;  // or the block-local order of the light rows
     int32_t step = 1;               // entries per step of the light-row loop (its step classes)
+    // Dense-tile windows (win_flags != nullptr): aligned 64-row windows whose
+    // light rows are estimated to hold >= tile_min entries inside the window
+    // are flagged for the tile kernel, and their light rows left out of the
+    // light-row order.  The estimate reads one entry of every 8th light row.
+    const int32_t* colidx = nullptr;
+    uint8_t* win_flags = nullptr;  // [ceil(N / 64)]
+    int32_t tile_min = 0;
 };
 
 struct MergeParams {
@@ -223,6 +237,18 @@ template <int HL> __device__ __forceinline__ float head_sum(float x) {
     if constexpr (HL >= 16) x += dpp<0x140>(x);  // row_mirror: other half of 16
     if constexpr (HL >= 32) x += __shfl_xor(x, 16);
     if constexpr (HL >= 64) x += __shfl_xor(x, 32);
+    return x;
+}
+
+// Sum of an int over the 64 lanes of a wavefront, in every lane (the head_sum
+// pattern: DPP within rows of 16 lanes, then two cross-row swaps).
+__device__ __forceinline__ int wave_sum_i32(int x) {
+    x += __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);   // lane ^ 1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);   // lane ^ 2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false);  // other quad of 8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false);  // other half of 16
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
     return x;
 }
 
@@ -307,11 +333,14 @@ struct RowState {
     // value rows (paired with v_perm), accumulating in fp32.  Against widening
     // every element to fp32 this halves the vector instructions per entry.  The
     // normaliser sums the fp32 weights, so lse keeps fp32 accuracy; the rounded
-    // weights sum to within 2^-9 of it, which bounds the extra error of out by
-    // 2^-9 * sum_e p_e |v_e| / sum_e p_e.  (GATv2 widens its gathered rows for
+    // weights differ from it by at most the bf16 unit roundoff 2^-8 each, which
+    // bounds the extra error of out by 2^-8 * sum_e p_e |v_e| / sum_e p_e.  (GATv2 widens its gathered rows for
     // the score anyway, and reusing them for P*V measured faster than pairs.)
+    // KIND_GT_WF32 keeps the dot2 score but multiplies fp32 weights with the
+    // widened value rows.
     static constexpr bool kDot2 = std::is_same<T, bf16_tag>::value && !kGat;
-    static_assert(!kDot2 || kU % 2 == 0, "dot2 pairs entries");
+    static constexpr bool kPairPV = kDot2 && KIND == KIND_GT;
+    static_assert(!kPairPV || kU % 2 == 0, "dot2 pairs entries");
     float q[Gm::kNV][Gm::kEPV];
     float a[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
     float a2[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
@@ -437,7 +466,7 @@ struct RowState {
             l[k] *= corr;
 #pragma unroll
             for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] *= corr;
-            if constexpr (kDot2) {
+            if constexpr (kPairPV) {
 #pragma unroll
                 for (int u = 0; u < U; u += 2) {
                     const float p0 = fast_exp2(s[u][k] - mb), p1 = fast_exp2(s[u + 1][k] - mb);
@@ -695,8 +724,10 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
     const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
     const int g = lane / Gm::kG, lig = lane % Gm::kG;
-    if (!p.skip_light) light_rows<T, H, D, KIND>(p, lo + lw, hi, waves_per_xcd, g, lig,
-                                                  tile + g * LightTile<Gm::kG>::kEntries);
+    // (with a light-row order, its count can be zero: every light row lies in
+    // a dense window of the tile kernel)
+    if (SortedLight<T, H, D, KIND>::value && CNT(p.counters, CNT_LIGHT) == 0) return;
+    light_rows<T, H, D, KIND>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * LightTile<Gm::kG>::kEntries);
 }
 
 // ------------------------------------------------------- dense-tile path
@@ -704,17 +735,21 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
 // Locally dense windows (Section 3.3 and Appendix D.3 of the paper pack local
 // neighbourhoods into tiles for matrix cores; this is a gfx950 design of the
 // same idea, not the paper's 16x8 TCB format).  Rows are grouped in aligned
-// windows of 64; the window's own 64 ids are its tile columns.  In tile mode
-// this kernel handles every light row (one workgroup per window):
-//   1. stage the window's rowptr, the CSR entries of its light rows, its K
-//      rows and its V rows (transposed) in LDS with independent loads;
+// windows of 64; the window's own 64 ids are its tile columns.  The partition
+// kernel lists the windows whose light rows it estimates to be dense (a
+// sample of one entry in every 8th light row); this kernel takes every light
+// row of a listed window (a workgroup per window, looping over the list),
+// the CSR kernel every other row:
+//   1. stage the window's rowptr, its K rows and its V rows (transposed) in
+//      LDS with independent loads, and each light row's entries in registers;
 //   2. per light row, a 64-bit mask of its in-window entries (a row with a
 //      repeated in-window entry cannot be a mask and does not use the tile);
 //   3. if the window holds at least `min_entries` masked entries, per head and
 //      per 16-row strip (one wave each):
 //        S^T = K_w Q_strip^T  (bf16 MFMA 16x16x32, fp32 accumulate),
 //      masked row-wise softmax statistics, and acc = P V_w (second MFMA, P
-//      rounded to bf16; the normaliser sums the same rounded weights);
+//      rounded to bf16, as in the CSR step of bf16 rows; the normaliser and
+//      lse sum the fp32 weights);
 //   4. every light row then streams its remaining entries (all of them for a
 //      row without a tile) with the CSR online-softmax step, continuing from
 //      the tile's (m, l, acc), and writes its output.
@@ -730,7 +765,11 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWin = 64;          // window rows = tile columns
 constexpr int kWinMaxDeg = 64;    // light rows handled here have at most this degree
-constexpr int kVtStride = 72;     // padded row of the transposed V tile (bf16 elements)
+// Padded row of the transposed V tile, in bf16 elements: 34 dwords, so that
+// the 16 rows one P*V operand load reads (8 bytes per lane) start 2 banks
+// apart and cover all 32 banks once (a 36-dword row put rows n and n + 8 on
+// the same banks).
+constexpr int kVtStride = 68;
 
 struct TileParams {
     const int64_t* rowptr;
@@ -744,6 +783,8 @@ struct TileParams {
     float c;  // scale * log2(e)
     int32_t light_max;  // <= kWinMaxDeg
     int32_t min_entries;
+    const uint8_t* win_flags;  // [ceil(N / 64)]: 1 for the dense windows the partition found
+    const int32_t* counters;   // CNT_WIN: how many there are
 };
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
@@ -781,20 +822,35 @@ struct TileWaves {
     static constexpr int value = H <= 2 ? 4 : 1;
 };
 
-template <int H, int D>
+template <int H, int D, int KIND>
 __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(TileWaves<H, D>::value)))
 gt_tile_kernel(TileParams p) {
     using Gm = Geo<bf16_tag, H, D>;
     using L = TileLds<H, D>;
+    using RS = RowState<bf16_tag, H, D, KIND>;
     constexpr int HD = H * D;
-    constexpr int G = Gm::kG, P = Gm::kP, U = RowState<bf16_tag, H, D>::kU;
+    constexpr int G = Gm::kG, P = Gm::kP, U = RS::kU;
+    // fp32 weights (KIND_GT_WF32): P = hi + lo as two bf16 terms, two P*V
+    // products; |P - hi - lo| <= 2^-17 P
+    constexpr bool kSplitP = KIND == KIND_GT_WF32;
     static_assert(HD <= 128 && D % 32 == 0, "tile path shapes");
     __shared__ __attribute__((aligned(16))) L lds;
 
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
     const int g16 = lane >> 4, n16 = lane & 15;  // MFMA lane coordinates
+    // Workgroup b takes window b if the partition flagged it dense and returns
+    // at once otherwise.  The count of dense windows (one word every
+    // workgroup reads) and the window's flag are loaded first and checked
+    // after the row-bound loads are issued, so a dense window waits on one
+    // round trip, and a graph without dense windows ends each workgroup on
+    // a cached word.  (A persistent loop over a list of the dense windows
+    // measured slower: it raised the kernel's register pressure past its
+    // 128-VGPR budget and spilled; a list also needs its entry before any
+    // other load.)
     const int64_t r0 = (int64_t)blockIdx.x * kWin;
     const int64_t wend = r0 + kWin;
+    const int32_t n_dense = CNT(p.counters, CNT_WIN);
+    const uint8_t flagged = p.win_flags[blockIdx.x];
 
     // bounds of this lane's row in the mask stage (4 lanes per row), loaded
     // first so that its entries can be requested right after the staging loads
@@ -806,6 +862,7 @@ gt_tile_kernel(TileParams p) {
         mb = p.rowptr[r];
         me = p.rowptr[r + 1];
     }
+    if (n_dense == 0 || !flagged) return;
 
     // ---- 1. staging
     if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
@@ -922,13 +979,15 @@ gt_tile_kernel(TileParams p) {
                 m = fmaxf(m, __shfl_xor(m, 16));
                 m = fmaxf(m, __shfl_xor(m, 32));
             }
-            uint32_t pb[16];
+            uint32_t pb[16], pl[kSplitP ? 16 : 1];
             float ls = 0.0f;
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
                 const float pv = (m == -INFINITY) ? 0.0f : fast_exp2(pr[t] - m);
                 pb[t] = bf16_rne(pv);
-                ls += __uint_as_float(pb[t] << 16);
+                // pv - hi is exact in fp32; its bf16 rounding is the low term
+                if constexpr (kSplitP) pl[t] = bf16_rne(pv - __uint_as_float(pb[t] << 16));
+                ls += pv;  // the normaliser (and lse) from the fp32 weights
             }
             ls += __shfl_xor(ls, 16);
             ls += __shfl_xor(ls, 32);
@@ -943,6 +1002,11 @@ gt_tile_kernel(TileParams p) {
                 const uint4 au = make_uint4(pb[8 * ks + 0] | (pb[8 * ks + 1] << 16), pb[8 * ks + 2] | (pb[8 * ks + 3] << 16),
                                             pb[8 * ks + 4] | (pb[8 * ks + 5] << 16), pb[8 * ks + 6] | (pb[8 * ks + 7] << 16));
                 const bf16x8_t ap = __builtin_bit_cast(bf16x8_t, au);
+                bf16x8_t apl = ap;
+                if constexpr (kSplitP)
+                    apl = __builtin_bit_cast(
+                        bf16x8_t, make_uint4(pl[8 * ks + 0] | (pl[8 * ks + 1] << 16), pl[8 * ks + 2] | (pl[8 * ks + 3] << 16),
+                                             pl[8 * ks + 4] | (pl[8 * ks + 5] << 16), pl[8 * ks + 6] | (pl[8 * ks + 7] << 16)));
 #pragma unroll
                 for (int dt = 0; dt < D / 16; ++dt) {
                     const int e = h * D + 16 * dt + n16;
@@ -950,6 +1014,8 @@ gt_tile_kernel(TileParams p) {
                     const uint2 hi = *reinterpret_cast<const uint2*>(&lds.big.kv.vt[e][32 * ks + 16 + 4 * g16]);
                     const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
                     oacc[h][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bv, oacc[h][dt], 0, 0, 0);
+                    if constexpr (kSplitP)
+                        oacc[h][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(apl, bv, oacc[h][dt], 0, 0, 0);
                 }
             }
         }
@@ -997,7 +1063,7 @@ gt_tile_kernel(TileParams p) {
         const bool use_tile = dense && ((ok_bits >> (4 * sr)) & 1ull);
         const int wr = 16 * wv + sr;
         const int64_t row = r0 + wr;
-        RowState<bf16_tag, H, D> st;
+        RS st;
         st.begin(p.Q, row, lig);
         if (use_tile) {
 #pragma unroll
@@ -1079,6 +1145,7 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock], scan_s[kWavesPerBlock];
     __shared__ int base[4];
     __shared__ int cls_cnt[kLightClasses], cls_pos[kLightClasses];
+    __shared__ int win_dense[kPartRowsPerThread][kWavesPerBlock];  // dense-tile window flags of this block
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const int64_t r0 = (int64_t)blockIdx.x * kPartRowsPerBlock;
     int64_t rb[kPartRowsPerThread], deg[kPartRowsPerThread];
@@ -1105,6 +1172,50 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
             n_slot += nch > 1 ? nch : 0;
         }
     }
+    // Dense-tile windows.  In iteration k, wave wv holds the 64 rows of one
+    // aligned window (r0 is a multiple of 1024).  The window's light rows hold
+    // ld entries; every 8th light row contributes its middle entry as a
+    // sample, and the in-window share of the sampled rows' entries (self-loops
+    // not counted) estimates the window's in-window entries (the tile kernel
+    // counts them exactly and still streams a window that falls short).  A dense window's light rows
+    // belong to the tile kernel (tiled), all others stay on this path.
+    bool tiled[kPartRowsPerThread];
+#pragma unroll
+    for (int k = 0; k < kPartRowsPerThread; ++k) tiled[k] = false;
+    if (p.win_flags) {
+        int32_t smp[kPartRowsPerThread];
+#pragma unroll
+        for (int k = 0; k < kPartRowsPerThread; ++k) {
+            const int64_t r = r0 + k * kBlock + threadIdx.x;
+            smp[k] = -1;
+            if (r < p.N && deg[k] > 0 && deg[k] <= p.light_max && (lane & 7) == 0)
+                smp[k] = p.colidx[rb[k] + deg[k] / 2];
+        }
+#pragma unroll
+        for (int k = 0; k < kPartRowsPerThread; ++k) {
+            const int64_t r = r0 + k * kBlock + threadIdx.x;
+            const bool lt = r < p.N && deg[k] <= p.light_max;
+            // light degrees are <= 64, so a window's sums fit: ld <= 4096 and
+            // the sampled sums (8 rows) <= 512, packed two to a word
+            const int ld = wave_sum_i32(lt ? (int)deg[k] : 0);
+            // a sampled self-loop does not count: every row has at most one,
+            // and rows holding only their self-loop would make sparse windows
+            // look dense
+            const int sd = smp[k] >= 0 ? (int)deg[k] : 0;
+            const int si = (smp[k] >= 0 && smp[k] != r && ((int64_t)smp[k] >> 6) == (r >> 6)) ? sd : 0;
+            const int ss = wave_sum_i32(sd | (si << 16));
+            const int sd_w = ss & 0xFFFF, si_w = ss >> 16;
+            const bool dense = p.tile_min <= 1 ? ld > 0
+                                               : (ld >= p.tile_min && si_w > 0 &&
+                                                  (int64_t)si_w * ld >= (int64_t)p.tile_min * sd_w);
+            tiled[k] = dense && lt;
+            const int64_t win = (r0 + k * kBlock + wv * kWave) >> 6;
+            if (lane == 0) {
+                if (win * kWave < p.N) p.win_flags[win] = dense ? 1 : 0;
+                win_dense[k][wv] = dense ? 1 : 0;
+            }
+        }
+    }
     if (p.light_list) {
         // Light rows of this block in descending step count (a counting sort in
         // LDS), so the lane groups of a wave take rows of similar length and a
@@ -1120,7 +1231,7 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
         for (int k = 0; k < kPartRowsPerThread; ++k) {
             const int64_t r = r0 + k * kBlock + threadIdx.x;
             cls[k] = -1;
-            if (r < p.N && deg[k] <= p.light_max) {
+            if (r < p.N && deg[k] <= p.light_max && !tiled[k]) {
                 const int64_t st = (deg[k] + p.step - 1) / p.step;
                 cls[k] = (int)(st < kLightClasses - 1 ? st : kLightClasses - 1);
                 atomicAdd(&cls_cnt[cls[k]], 1);
@@ -1158,6 +1269,15 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
         base[1] = tot_h ? atomicAdd(&CNT(p.counters, CNT_HEAVY), tot_h) : 0;
         base[2] = tot_c ? atomicAdd(&CNT(p.counters, CNT_CHUNKS), tot_c) : 0;
         base[3] = tot_s ? atomicAdd(&CNT(p.counters, CNT_SLOTS), tot_s) : 0;
+        // light rows left in the order: zero lets the attention kernel skip
+        // its light-row loop (every light row in dense windows)
+        if (p.light_list && cls_cnt[0]) atomicAdd(&CNT(p.counters, CNT_LIGHT), cls_cnt[0]);
+        if (p.win_flags) {
+            int n_dense = 0;
+            for (int k = 0; k < kPartRowsPerThread; ++k)
+                for (int w = 0; w < kWavesPerBlock; ++w) n_dense += win_dense[k][w];
+            if (n_dense) atomicAdd(&CNT(p.counters, CNT_WIN), n_dense);
+        }
     }
     __syncthreads();
     int pos = base[0];
@@ -1520,8 +1640,10 @@ PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
 // fp32 4x32 features, 16K nodes took 76 us per call at 1024 against 48 us at
 // 256, and 65K nodes 114 us against 95 us at 512.  The default keeps a chunk's
 // steps within half the time the call's gathers take at ~7 TB/s, in multiples
-// of 64, capped at 1024, the measured best on large graphs (the bench graph,
-// 169K nodes, and every larger one get 1024).
+// of 64, capped at 1024, the measured best on large graphs.  With the
+// graph-transformer forward (two gathered rows per entry) the arxiv-shaped
+// 169K-node graph and every larger one get 1024; the GATv2 forward, one
+// gathered row per entry, gets 768 there and 1024 from about twice its size.
 int default_chunk(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
     constexpr double kGatherBytesPerSecond = 7.0e12, kStepSeconds = 1.0e-6;
     const double gather_seconds = (double)E * (double)bytes_per_entry / kGatherBytesPerSecond;
@@ -1556,6 +1678,8 @@ int attn_blocks_per_cu(int dev) {
     return cache[dev];
 }
 
+constexpr int kDefaultTileMin = 256;
+
 template <typename T, int H, int D, int KIND>
 gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
@@ -1570,12 +1694,17 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     // would give 384 entries there, 5.7 % slower.
     int light_max = 8 * Gm::kU;
     int heavy_min = 256;
-    int chunk = default_chunk(a.E, (KIND == KIND_GT ? 2 : 1) * Gm::kRowBytes,
+    int chunk = default_chunk(a.E, (KIND != KIND_GATV2 ? 2 : 1) * Gm::kRowBytes,
                               Gm::kP * StepOf<T, H, D, KIND_GT>::value);
     int grid = 0;
-    int tile_min = 0;  // dense-tile windows off
+    // Dense-tile windows (tile shapes only): on by default, for windows
+    // estimated to hold at least 256 in-window entries, which a 64-row block
+    // at half density holds about eight times over (measured on the SBM
+    // workload; on the R-MAT one no window qualifies and the tile kernel
+    // finds an empty list).
+    int tile_min = kDefaultTileMin;
     if (tu) {
-        if (tu->dense_tiles > 0) tile_min = tu->dense_tiles;
+        if (tu->dense_tiles != 0) tile_min = tu->dense_tiles;  // < 0: off
         if (tu->light_max_deg > 0) light_max = tu->light_max_deg;
         if (tu->heavy_min_deg > 0) heavy_min = tu->heavy_min_deg;
         if (tu->chunk_edges > 0) chunk = (tu->chunk_edges + kWave - 1) / kWave * kWave;
@@ -1583,17 +1712,15 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     }
     if (heavy_min <= light_max) heavy_min = light_max + 1;
     constexpr bool kTileShape =
-        KIND == KIND_GT && std::is_same<T, bf16_tag>::value && H * D <= 128 && D % 32 == 0;
+        KIND != KIND_GATV2 && std::is_same<T, bf16_tag>::value && H * D <= 128 && D % 32 == 0;
+    static_assert(!kTileShape || SortedLight<T, H, D, KIND>::value,
+                  "the tile path leaves its rows out of the light-row order");
     const bool tiles = kTileShape && tile_min > 0;
     if (tiles && light_max > kWinMaxDeg) light_max = kWinMaxDeg;
 
     int dev = 0;
     hipError_t he = hipGetDevice(&dev);
     if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
-    if (grid <= 0 && tiles) {
-        // light rows belong to the tile kernel: only the wave items remain
-        grid = 4 * device_cus(dev) * attn_blocks_per_cu<T, H, D, KIND>(dev);
-    }
     if (grid <= 0) {
         // About two light items (P rows each) per wave, between 4x and 64x the
         // number of workgroups the device holds at once: finer than one
@@ -1620,7 +1747,10 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     const size_t o_ml = off;       off = align_up(off + (size_t)caps.slots * H * sizeof(float2), 256);
     const size_t o_acc = off;      off = align_up(off + (size_t)caps.slots * H * D * sizeof(float), 256);
     const size_t o_light = off;
-    off = align_up(off + ((tiles || !SortedLight<T, H, D, KIND>::value) ? 0 : (size_t)a.N * sizeof(int32_t)), 256);
+    off = align_up(off + (!SortedLight<T, H, D, KIND>::value ? 0 : (size_t)a.N * sizeof(int32_t)), 256);
+    const int64_t n_windows = (a.N + kWin - 1) / kWin;
+    const size_t o_win = off;
+    off = align_up(off + (tiles ? (size_t)n_windows : 0), 256);
     const size_t ws_bytes = off;
 
     CallWorkspace cw;
@@ -1648,8 +1778,13 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     pp.med_list = reinterpret_cast<int32_t*>(ws + o_med);
     pp.heavy = reinterpret_cast<HeavyRow*>(ws + o_heavy);
     pp.chunks = reinterpret_cast<ChunkItem*>(ws + o_chunks);
-    pp.light_list = (tiles || !SortedLight<T, H, D, KIND>::value) ? nullptr : reinterpret_cast<int32_t*>(ws + o_light);
+    pp.light_list = !SortedLight<T, H, D, KIND>::value ? nullptr : reinterpret_cast<int32_t*>(ws + o_light);
     pp.step = RowState<T, H, D, KIND>::kU;
+    if (tiles) {
+        pp.colidx = a.colidx;
+        pp.win_flags = reinterpret_cast<uint8_t*>(ws + o_win);
+        pp.tile_min = tile_min;
+    }
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
     ph.mark(1, stream);  // the attention phase includes the tile kernel
     if constexpr (kTileShape) {
@@ -1666,8 +1801,9 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
             tp.c = a.scale * 1.4426950408889634f;
             tp.light_max = light_max;
             tp.min_entries = tile_min;
-            const int tgrid = (int)((a.N + kWin - 1) / kWin);
-            hipLaunchKernelGGL((gt_tile_kernel<H, D>), dim3(tgrid), dim3(kBlock), 0, stream, tp);
+            tp.win_flags = pp.win_flags;
+            tp.counters = counters;
+            hipLaunchKernelGGL((gt_tile_kernel<H, D, KIND>), dim3((unsigned)n_windows), dim3(kBlock), 0, stream, tp);
             if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "tile launch");
         }
     }
@@ -1681,7 +1817,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.out = static_cast<char*>(a.out);
     ap.lse = a.lse;
     ap.N = a.N;
-    ap.c = (KIND == KIND_GT ? a.scale : 1.0f) * 1.4426950408889634f;
+    ap.c = (KIND != KIND_GATV2 ? a.scale : 1.0f) * 1.4426950408889634f;
     ap.att = a.att;
     ap.slope = a.slope;
     ap.light_max = light_max;
@@ -1691,7 +1827,6 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     ap.chunks = pp.chunks;
     ap.part_acc = reinterpret_cast<float*>(ws + o_acc);
     ap.part_ml = reinterpret_cast<float2*>(ws + o_ml);
-    ap.skip_light = tiles ? 1 : 0;
     ap.light_list = pp.light_list;
     hipLaunchKernelGGL((gt_attn_kernel<T, H, D, KIND>), dim3(grid), dim3(kBlock), 0, stream, ap);
     if ((he = hipGetLastError()) != hipSuccess) return hip_fail(he, "attention launch");
@@ -1738,8 +1873,23 @@ bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
     return x < y + bn && y < x + an;
 }
 
+// Tuning fields are counts of entries, rows or workgroups: positive values
+// beyond kTuningMax (about 2^31 - 2^16) would overflow the partition's
+// rounding and comparisons, so they are refused.
+constexpr int32_t kTuningMax = INT32_MAX - (1 << 16);
+
+gt_status check_tuning(const gt_tuning* tu) {
+    if (!tu) return GT_SUCCESS;
+    const int32_t f[] = {tu->light_max_deg, tu->heavy_min_deg, tu->chunk_edges, tu->grid_blocks, tu->dense_tiles};
+    for (int32_t v : f)
+        if (v > kTuningMax)
+            return fail(GT_ERROR_INVALID_VALUE, "a tuning field exceeds " + std::to_string(kTuningMax));
+    return GT_SUCCESS;
+}
+
 gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t stream) {
     t_last_error.clear();
+    if (check_tuning(tu) != GT_SUCCESS) return GT_ERROR_INVALID_VALUE;
     if (dtype != GT_DTYPE_F32 && dtype != GT_DTYPE_BF16) return fail(GT_ERROR_NOT_SUPPORTED, "unknown dtype");
     if (a.N < 0 || a.N >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "N must be in [0, 2^31)");
     if (a.E < 0 || a.E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
@@ -1750,7 +1900,9 @@ gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t st
     if (a.kind == KIND_GATV2)
         fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GATV2>(a.H, a.D) : pick_hd<bf16_tag, KIND_GATV2>(a.H, a.D);
     else
-        fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GT>(a.H, a.D) : pick_hd<bf16_tag, KIND_GT>(a.H, a.D);
+        fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GT>(a.H, a.D)
+             : (tu && tu->weights_fp32) ? pick_hd<bf16_tag, KIND_GT_WF32>(a.H, a.D)
+                                        : pick_hd<bf16_tag, KIND_GT>(a.H, a.D);
     if (!fn)
         return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +
                                                 std::to_string(a.D) + "); H in {1,2,4,8} with D in {32,64,128,256}, or bf16 D = 512 with H in {1,2,4}");
@@ -1824,6 +1976,7 @@ gt_status run_reduce(gt_dtype dtype, int op, const ReduceArgs& a0, const gt_tuni
     t_last_error.clear();
     if (dtype != GT_DTYPE_F32 && dtype != GT_DTYPE_BF16) return fail(GT_ERROR_NOT_SUPPORTED, "unknown dtype");
     if (op != GT_REDUCE_MIN && op != GT_REDUCE_MAX) return fail(GT_ERROR_NOT_SUPPORTED, "unknown reduce op");
+    if (check_tuning(tu) != GT_SUCCESS) return GT_ERROR_INVALID_VALUE;
     if (a0.N < 0 || a0.N >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "N must be in [0, 2^31)");
     if (a0.E < 0 || a0.E >= (int64_t(1) << 31)) return fail(GT_ERROR_INVALID_VALUE, "E must be in [0, 2^31)");
     if (a0.F < 1) return fail(GT_ERROR_INVALID_VALUE, "F must be positive");

@@ -65,6 +65,37 @@ def test_host_validation(lib, kw, status):
     assert lib.gt_last_error_message()
 
 
+@pytest.mark.parametrize("field", ["light_max_deg", "heavy_min_deg", "chunk_edges", "grid_blocks",
+                                   "dense_tiles"])
+def test_oversized_tuning_field_is_refused(lib, field):
+    # a count near INT32_MAX would overflow the partition's rounding: refused
+    # on the host, before any device work (the pointers are never touched)
+    import paper_2605_31500_amd as gt
+    P = ctypes.c_void_p
+    for value, status in (((1 << 31) - 1, 1), ((1 << 31) - (1 << 16) + 1, 1)):
+        tu = gt.GtTuning(**{field: value})
+        assert lib.gt_attn_fwd_ex(0, P(FAKE), P(FAKE), P(FAKE), P(FAKE + 0x100000), P(FAKE + 0x200000),
+                                  P(FAKE + 0x300000), None, 10, 20, 4, 32, ctypes.c_float(0.1),
+                                  ctypes.byref(tu), None) == status
+        assert b"tuning" in lib.gt_last_error_message()
+        assert lib.gt_segment_reduce(0, 0, P(FAKE), P(FAKE), P(FAKE), P(FAKE + 0x100000),
+                                     P(FAKE + 0x200000), 10, 20, 64, ctypes.byref(tu), None) == status
+
+
+@pytest.mark.parametrize("kw,status", [(dict(H=3), 2), (dict(N=-1), 1), (dict(out=FAKE), 1),
+                                       (dict(scale=float("nan")), 1)])
+def test_noalloc_entry_host_validation(lib, kw, status):
+    # the allocation-free entry point validates like gt_attn_fwd_ex
+    a = dict(dtype=0, rowptr=FAKE, colidx=FAKE, Q=FAKE, K=FAKE + 0x100000, V=FAKE + 0x200000,
+             out=FAKE + 0x300000, N=10, E=20, H=4, D=32, scale=0.1)
+    a.update(kw)
+    P = ctypes.c_void_p
+    assert lib.gt_attn_fwd_noalloc(a["dtype"], P(a["rowptr"]), P(a["colidx"]), P(a["Q"]), P(a["K"]), P(a["V"]),
+                                   P(a["out"]), None, a["N"], a["E"], a["H"], a["D"], ctypes.c_float(a["scale"]),
+                                   None, None) == status
+    assert lib.gt_last_error_message()
+
+
 def test_empty_graph_is_a_no_op(lib):
     # N == 0 enqueues nothing and touches no pointer
     assert call(lib, N=0, E=0, rowptr=FAKE) == 0

@@ -133,7 +133,7 @@ def test_lse_tile_mode():
     dO, _, _ = synth.features(36, N, 2, 64, "bf16")
     got = run_gpu_fwd_bwd(w_rp, w_ci, Q, K, V, dO, np.float32(0.125), tuning={"dense_tiles": 256})
     _, _, ref_lse = oracle.gt_attn_fwd(w_rp, w_ci, Q, K, V, np.float32(0.125), want_absagg=False)
-    check_lse(got[1], ref_lse, 4e-3)  # tile weights are rounded to bf16
+    check_lse(got[1], ref_lse, 1e-5)  # the tile normaliser sums the fp32 weights
 
 
 def check_grads_all(w, dO, got):

@@ -17,6 +17,7 @@ from tests.helpers import TOL_BF16, bf16_bits_to_f32, fwd_gate_error_all_rows, g
 pytestmark = pytest.mark.gpu
 
 TILE_SHAPES = [(1, 32), (1, 64), (1, 128), (2, 32), (2, 64), (4, 32)]
+CSR_ONLY = {"dense_tiles": -1}
 
 
 def csr_from_rows(rows):
@@ -61,9 +62,10 @@ def test_tiles_irregular(H, D):
     scale = np.float32(1 / math.sqrt(D))
     a = check(rowptr, colidx, Q, K, V, scale, tiles=256)
     check(rowptr, colidx, Q, K, V, scale, tiles=1)
-    # the tile path really ran: its bf16-rounded weights change some outputs
-    # in dense windows, and none in the sparse window 9 (CSR kernel there)
-    csr = run_gpu(rowptr, colidx, Q, K, V, scale)
+    # the tile path really ran: its products round differently from the CSR
+    # step's, which changes some outputs in dense windows, and none in the
+    # sparse window 9 (CSR kernel there)
+    csr = run_gpu(rowptr, colidx, Q, K, V, scale, tuning=CSR_ONLY)
     assert not np.array_equal(a[:64 * 9], csr[:64 * 9])
     assert np.array_equal(a[64 * 9:64 * 10], csr[64 * 9:64 * 10])
 
@@ -84,27 +86,56 @@ def test_tiles_deterministic_and_off_equivalence():
     b = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning={"dense_tiles": 256})
     assert np.array_equal(a, b)
     # a threshold no window reaches leaves everything to the CSR kernel
-    off = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125))
+    off = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning=CSR_ONLY)
     none = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning={"dense_tiles": 1 << 20})
     assert np.array_equal(off, none)
+    # the default is the tile path at threshold 256
+    assert np.array_equal(run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125)), a)
 
 
 def test_tiles_ignored_for_fp32_and_wide_rows():
     rowptr, colidx = irregular_block_graph(23)
     N = rowptr.size - 1
     Q, K, V = synth.features(23, N, 2, 64, "f32")
-    assert np.array_equal(run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125)),
+    assert np.array_equal(run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125), tuning=CSR_ONLY),
                           run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125),
                                   tuning={"dense_tiles": 256}))
     Qb, Kb, Vb = synth.features(23, N, 8, 64, "bf16")  # H*D = 512: no tile variant
-    assert np.array_equal(run_gpu(rowptr, colidx, Qb, Kb, Vb, np.float32(0.125)),
+    assert np.array_equal(run_gpu(rowptr, colidx, Qb, Kb, Vb, np.float32(0.125), tuning=CSR_ONLY),
                           run_gpu(rowptr, colidx, Qb, Kb, Vb, np.float32(0.125),
                                   tuning={"dense_tiles": 256}))
 
 
-def test_tiles_full_sbm_all_rows():
+@pytest.mark.parametrize("H,D", TILE_SHAPES)
+def test_tiles_weights_fp32(H, D):
+    """Tiles with fp32 weights (each weight as two bf16 terms, two P*V
+    products): only the bf16 output rounding (2^-8) and fp32-level terms are
+    left; lse to the fp32 tolerance."""
+    import torch
+    import paper_2605_31500_amd as gtm
+    from tests.helpers import to_device
+    rowptr, colidx = irregular_block_graph(H * 100 + D + 1)
+    N = rowptr.size - 1
+    Q, K, V = synth.features(H * 100 + D + 1, N, H, D, "bf16")
+    scale = np.float32(1 / math.sqrt(D))
+    dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    out = torch.empty_like(dev[2])
+    lse = torch.empty((N, H), dtype=torch.float32, device=out.device)
+    gtm.gt_attn_fwd_ex(*dev, out, scale, tuning={"dense_tiles": 1, "weights_fp32": 1}, lse=lse)
+    torch.cuda.synchronize()
+    got = bf16_bits_to_f32(out.view(torch.int16).cpu().numpy().view(np.uint16))
+    ref, absagg, ref_lse = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale)
+    assert gate_error(got, ref, absagg) <= 2.0 ** -8 + 1e-4
+    l = lse.cpu().numpy()
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isneginf(l), ~fin)
+    assert np.all(np.abs(l[fin] - ref_lse[fin]) <= 1e-5 * np.maximum(1.0, np.abs(ref_lse[fin])))
+
+
+def test_tiles_off_full_sbm_all_rows():
+    # the CSR kernel alone on the locally dense workload (tiles are the default there)
     w = workload(3)
-    got = run_gpu(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, tuning={"dense_tiles": 256})
+    got = run_gpu(w.rowptr, w.colidx, w.Q, w.K, w.V, w.scale, tuning=CSR_ONLY)
     assert np.all(np.isfinite(got))
     err = fwd_gate_error_all_rows(w, got)
     print("gate error %.3g" % err, flush=True)
