@@ -1112,24 +1112,37 @@ gt_tile_kernel(TileParams p) {
 constexpr int kMaxChunks = 32;
 constexpr int kLightClasses = 16;  // step-count classes of the light-row order
 
-__device__ __forceinline__ int block_exclusive_scan(int v, int* lds_waves, int* total) {
+// Exclusive scans over the block of three per-thread counts at once (one
+// barrier); totals in tot[0..2].
+__device__ __forceinline__ int3 block_exclusive_scan3(int3 v, int3* lds_waves, int* tot) {
     const int lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
-    int x = v;
+    int3 x = v;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
-        const int y = __shfl_up(x, o);
-        if (lane >= o) x += y;
+        const int a = __shfl_up(x.x, o), b = __shfl_up(x.y, o), c = __shfl_up(x.z, o);
+        if (lane >= o) {
+            x.x += a;
+            x.y += b;
+            x.z += c;
+        }
     }
     if (lane == kWave - 1) lds_waves[wv] = x;
     __syncthreads();
-    int before = 0, sum = 0;
+    int3 before = make_int3(0, 0, 0);
+    tot[0] = tot[1] = tot[2] = 0;
 #pragma unroll
     for (int w = 0; w < kWavesPerBlock; ++w) {
-        if (w < wv) before += lds_waves[w];
-        sum += lds_waves[w];
+        const int3 t = lds_waves[w];
+        if (w < wv) {
+            before.x += t.x;
+            before.y += t.y;
+            before.z += t.z;
+        }
+        tot[0] += t.x;
+        tot[1] += t.y;
+        tot[2] += t.z;
     }
-    *total = sum;
-    return before + x - v;
+    return make_int3(before.x + x.x - v.x, before.y + x.y - v.y, before.z + x.z - v.z);
 }
 
 __device__ __forceinline__ int chunks_of(int64_t deg, int chunk) {
@@ -1142,7 +1155,7 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     constexpr int kPartRowsPerThread = RPT;
     constexpr int kPartRowsPerBlock = kBlock * RPT;
     __shared__ int wave_cnt[kPartRowsPerThread][kWavesPerBlock];
-    __shared__ int scan_h[kWavesPerBlock], scan_c[kWavesPerBlock], scan_s[kWavesPerBlock];
+    __shared__ int3 scan3[kWavesPerBlock];
     __shared__ int base[4];
     __shared__ int cls_cnt[kLightClasses], cls_pos[kLightClasses];
     __shared__ int win_dense[kPartRowsPerThread][kWavesPerBlock];  // dense-tile window flags of this block
@@ -1257,27 +1270,33 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
         const int64_t rows_here = (p.N - r0 < kPartRowsPerBlock) ? p.N - r0 : kPartRowsPerBlock;
         for (int64_t j = n_light_rows + threadIdx.x; j < rows_here; j += kBlock) p.light_list[r0 + j] = -1;
     }
-    int tot_h, tot_c, tot_s;
-    const int off_h = block_exclusive_scan(n_heavy, scan_h, &tot_h);
-    const int off_c = block_exclusive_scan(n_chunk, scan_c, &tot_c);
-    const int off_s = block_exclusive_scan(n_slot, scan_s, &tot_s);
-    if (threadIdx.x == 0) {
-        int tot_m = 0;
-        for (int k = 0; k < kPartRowsPerThread; ++k)
-            for (int w = 0; w < kWavesPerBlock; ++w) tot_m += wave_cnt[k][w];
-        base[0] = tot_m ? atomicAdd(&CNT(p.counters, CNT_MED), tot_m) : 0;
-        base[1] = tot_h ? atomicAdd(&CNT(p.counters, CNT_HEAVY), tot_h) : 0;
-        base[2] = tot_c ? atomicAdd(&CNT(p.counters, CNT_CHUNKS), tot_c) : 0;
-        base[3] = tot_s ? atomicAdd(&CNT(p.counters, CNT_SLOTS), tot_s) : 0;
-        // light rows left in the order: zero lets the attention kernel skip
-        // its light-row loop (every light row in dense windows)
-        if (p.light_list && cls_cnt[0]) atomicAdd(&CNT(p.counters, CNT_LIGHT), cls_cnt[0]);
-        if (p.win_flags) {
-            int n_dense = 0;
+    int tots[3];
+    const int3 offs = block_exclusive_scan3(make_int3(n_heavy, n_chunk, n_slot), scan3, tots);
+    const int off_h = offs.x, off_c = offs.y, off_s = offs.z;
+    // The block's reservations: lanes 0..5 of wave 0 each add to one counter,
+    // so the atomics go out together rather than one after another.
+    if (threadIdx.x < 6) {
+        const int t = threadIdx.x;
+        int amount = 0, which = CNT_MED;
+        if (t == 0) {
             for (int k = 0; k < kPartRowsPerThread; ++k)
-                for (int w = 0; w < kWavesPerBlock; ++w) n_dense += win_dense[k][w];
-            if (n_dense) atomicAdd(&CNT(p.counters, CNT_WIN), n_dense);
+                for (int w = 0; w < kWavesPerBlock; ++w) amount += wave_cnt[k][w];
+        } else if (t < 4) {
+            amount = tots[t - 1];
+            which = t == 1 ? CNT_HEAVY : t == 2 ? CNT_CHUNKS : CNT_SLOTS;
+        } else if (t == 4) {
+            // light rows left in the order: zero lets the attention kernel
+            // skip its light-row loop (every light row in dense windows)
+            amount = p.light_list ? cls_cnt[0] : 0;
+            which = CNT_LIGHT;
+        } else {
+            if (p.win_flags)
+                for (int k = 0; k < kPartRowsPerThread; ++k)
+                    for (int w = 0; w < kWavesPerBlock; ++w) amount += win_dense[k][w];
+            which = CNT_WIN;
         }
+        const int b = amount ? atomicAdd(&CNT(p.counters, which), amount) : 0;
+        if (t < 4) base[t] = b;
     }
     __syncthreads();
     int pos = base[0];
