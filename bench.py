@@ -339,9 +339,9 @@ def pv_weights(w, args) -> str:
     """How a bf16 line multiplies softmax weights with value rows."""
     if args.gatv2:
         return "fp32 weights x widened value rows"
-    if args.weights_fp32:
-        return "fp32 weights x widened value rows (dense tiles: two bf16 terms per weight)"
-    return "weights rounded to bf16 before P*V (fp32 accumulation; normaliser from fp32 weights)"
+    if args.bf16_weights:
+        return "weights rounded to bf16 before P*V (fp32 accumulation; normaliser from fp32 weights)"
+    return "fp32 weights x widened value rows (dense tiles: two bf16 terms per weight)"
 
 
 def gatv2_attention_vector(w, seed: int):
@@ -615,8 +615,8 @@ def main() -> int:
                     help="threshold of the matrix-core path for dense 64-id windows (bf16, "
                          "H*D <= 128): windows estimated to hold at least MIN in-window entries; "
                          "0 = the library default (256), -1 = off")
-    ap.add_argument("--weights-fp32", action="store_true",
-                    help="bf16 features: keep the softmax weights in fp32 for P*V (gt_tuning.weights_fp32)")
+    ap.add_argument("--bf16-weights", action="store_true",
+                    help="bf16 features: round the softmax weights to bf16 for P*V (gt_tuning.bf16_weights)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run plain device-to-device copies of MIB "
                          "MiB (reference kernel for scaling HBM byte counters)")
@@ -659,8 +659,8 @@ def main() -> int:
     tuning = {}
     if args.dense_tiles:
         tuning["dense_tiles"] = args.dense_tiles
-    if args.weights_fp32:
-        tuning["weights_fp32"] = 1
+    if args.bf16_weights:
+        tuning["bf16_weights"] = 1
     tuning = tuning or None
     att = gatv2_attention_vector(w, args.config) if args.gatv2 else None
     if args.gatv2:

@@ -90,9 +90,9 @@ gt_status gt_attn_fwd(const int64_t* rowptr, const int32_t* colidx, const float*
 /*
  * bf16 features given as uint16 bit patterns; fp32 accumulation; bf16 output
  * rounded to nearest even.  Scores are bf16 dot products accumulated in fp32;
- * each softmax weight is rounded to bf16 before it multiplies its value row,
- * while the normaliser (and lse) sums the fp32 weights; the largest weight of
- * a row is exactly 1, so a single-entry row returns its value exactly.
+ * the fp32 softmax weights multiply the exactly widened value rows (in dense
+ * tiles, each weight as the sum of two bf16 terms); the largest weight of a
+ * row is exactly 1, so a single-entry row returns its value exactly.
  * Otherwise identical to gt_attn_fwd.
  */
 gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const uint16_t* Q,
@@ -134,18 +134,18 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  *                   of a listed window are computed by the tile kernel: their
  *                   in-window entries as masked 64x64 tiles with bf16 MFMA
  *                   (scores and P*V), then each row's remaining entries
- *                   streamed; all other rows by the CSR kernel.  Softmax
- *                   weights inside tiles are rounded to bf16 before the P*V
- *                   product, as in the CSR step of bf16 rows; the normaliser
- *                   and lse sum the fp32 weights.
- *   weights_fp32  : bf16 features only (ignored for fp32).  0 (default):
- *                   each softmax weight is rounded to bf16 before it
- *                   multiplies its value row (P*V in bf16 products, fp32
- *                   accumulation; out is then within 2^-8 sum_e alpha_e |v_e|
- *                   of the fp32-weight result).  Nonzero: the weights stay
- *                   fp32 and multiply the exactly widened value rows in fp32
- *                   (in dense tiles: each weight as the sum of two bf16 terms,
- *                   exact to 2^-17 relative, with two P*V products).
+ *                   streamed; all other rows by the CSR kernel.  The
+ *                   normaliser and lse sum the fp32 weights (for P*V see
+ *                   bf16_weights).
+ *   bf16_weights  : bf16 features only (ignored for fp32).  0 (default):
+ *                   the softmax weights stay fp32 and multiply the exactly
+ *                   widened value rows in fp32 (in dense tiles: each weight
+ *                   as the sum of two bf16 terms, exact to 2^-17 relative,
+ *                   with two P*V products).  Nonzero: each weight is rounded
+ *                   to bf16 before it multiplies its value row, two entries
+ *                   per bf16 dot2 (fewer vector instructions where the step
+ *                   is arithmetic-bound); out is then within
+ *                   2^-8 sum_e alpha_e |v_e| of the fp32-weight result.
  * Fields above 2^31 - 2^16 are refused (GT_ERROR_INVALID_VALUE).
  * Results are bitwise reproducible for fixed settings; different settings
  * change only the rounding.
@@ -156,7 +156,7 @@ typedef struct gt_tuning {
     int32_t chunk_edges;
     int32_t grid_blocks;
     int32_t dense_tiles;
-    int32_t weights_fp32;
+    int32_t bf16_weights;
 } gt_tuning;
 
 /*

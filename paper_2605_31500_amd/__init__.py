@@ -35,7 +35,7 @@ EXPORTED_SYMBOLS = (
 class GtTuning(ctypes.Structure):
     _fields_ = [("light_max_deg", ctypes.c_int32), ("heavy_min_deg", ctypes.c_int32),
                 ("chunk_edges", ctypes.c_int32), ("grid_blocks", ctypes.c_int32),
-                ("dense_tiles", ctypes.c_int32), ("weights_fp32", ctypes.c_int32)]
+                ("dense_tiles", ctypes.c_int32), ("bf16_weights", ctypes.c_int32)]
 
 
 class GtError(RuntimeError):

@@ -71,9 +71,10 @@ constexpr int kXcds = 8;
 // of each call.  Each counter sits on its own 256-byte line so that atomics
 // on different counters do not serialise on one cache line.
 // Score kinds of the attention skeleton.
-// KIND_GT_WF32: the graph-transformer score with the softmax weights kept in
-// fp32 for P*V (bf16 rows widen their value rows instead of pairing entries).
-enum { KIND_GT = 0, KIND_GATV2 = 1, KIND_GT_WF32 = 2 };
+// KIND_GT_BF16W: the graph-transformer score with each softmax weight rounded
+// to bf16 for P*V (bf16 rows pair two entries per dot2 instead of widening
+// their value rows); an option for rows whose steps are arithmetic-bound.
+enum { KIND_GT = 0, KIND_GATV2 = 1, KIND_GT_BF16W = 2 };
 
 // CNT_LIGHT: light rows left in the light-row order (shapes that build one);
 // CNT_WIN: dense-tile windows flagged by the partition.
@@ -328,18 +329,18 @@ struct RowState {
     static constexpr int kU = StepOf<T, H, D, KIND>::value;
     static constexpr bool kGat = KIND == KIND_GATV2;
     // bf16 graph-transformer rows: scores are bf16 dot2 on the raw Q and K
-    // pairs, and P*V pairs two entries: their weights are rounded to one bf16
-    // pair and a dot2 multiplies it with the same element of the two entries'
-    // value rows (paired with v_perm), accumulating in fp32.  Against widening
-    // every element to fp32 this halves the vector instructions per entry.  The
-    // normaliser sums the fp32 weights, so lse keeps fp32 accuracy; the rounded
-    // weights differ from it by at most the bf16 unit roundoff 2^-8 each, which
-    // bounds the extra error of out by 2^-8 * sum_e p_e |v_e| / sum_e p_e.  (GATv2 widens its gathered rows for
-    // the score anyway, and reusing them for P*V measured faster than pairs.)
-    // KIND_GT_WF32 keeps the dot2 score but multiplies fp32 weights with the
-    // widened value rows.
+    // pairs, accumulated in fp32 (the products of bf16 pairs are exact).  P*V
+    // widens the value rows exactly and multiplies them with the fp32 weights.
+    // KIND_GT_BF16W pairs two entries instead: their weights are rounded to
+    // one bf16 pair and a dot2 multiplies it with the same element of the two
+    // entries' value rows (paired with v_perm), accumulating in fp32; that
+    // halves the vector instructions of P*V, and each rounded weight is off by
+    // at most the bf16 unit roundoff 2^-8, which bounds the extra error of out
+    // by 2^-8 * sum_e p_e |v_e| / sum_e p_e.  Either way the normaliser (and
+    // lse) sums the fp32 weights.  (GATv2 widens its gathered rows for the
+    // score anyway.)
     static constexpr bool kDot2 = std::is_same<T, bf16_tag>::value && !kGat;
-    static constexpr bool kPairPV = kDot2 && KIND == KIND_GT;
+    static constexpr bool kPairPV = kDot2 && KIND == KIND_GT_BF16W;
     static_assert(!kPairPV || kU % 2 == 0, "dot2 pairs entries");
     float q[Gm::kNV][Gm::kEPV];
     float a[kGat ? Gm::kNV : 1][kGat ? Gm::kEPV : 1];
@@ -747,9 +748,10 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
 //   3. if the window holds at least `min_entries` masked entries, per head and
 //      per 16-row strip (one wave each):
 //        S^T = K_w Q_strip^T  (bf16 MFMA 16x16x32, fp32 accumulate),
-//      masked row-wise softmax statistics, and acc = P V_w (second MFMA, P
-//      rounded to bf16, as in the CSR step of bf16 rows; the normaliser and
-//      lse sum the fp32 weights);
+//      masked row-wise softmax statistics, and acc = P V_w (MFMA with P as
+//      the sum of two bf16 terms, so the weights keep 16 significant bits;
+//      with the bf16-weight option, one MFMA on P rounded to bf16); the
+//      normaliser and lse sum the fp32 weights;
 //   4. every light row then streams its remaining entries (all of them for a
 //      row without a tile) with the CSR online-softmax step, continuing from
 //      the tile's (m, l, acc), and writes its output.
@@ -830,9 +832,9 @@ gt_tile_kernel(TileParams p) {
     using RS = RowState<bf16_tag, H, D, KIND>;
     constexpr int HD = H * D;
     constexpr int G = Gm::kG, P = Gm::kP, U = RS::kU;
-    // fp32 weights (KIND_GT_WF32): P = hi + lo as two bf16 terms, two P*V
-    // products; |P - hi - lo| <= 2^-17 P
-    constexpr bool kSplitP = KIND == KIND_GT_WF32;
+    // fp32 weights (KIND_GT): P = hi + lo as two bf16 terms, two P*V
+    // products, |P - hi - lo| <= 2^-17 P; KIND_GT_BF16W: P rounded to bf16
+    constexpr bool kSplitP = KIND == KIND_GT;
     static_assert(HD <= 128 && D % 32 == 0, "tile path shapes");
     __shared__ __attribute__((aligned(16))) L lds;
 
@@ -1920,7 +1922,7 @@ gt_status run(gt_dtype dtype, const Args& a, const gt_tuning* tu, hipStream_t st
         fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GATV2>(a.H, a.D) : pick_hd<bf16_tag, KIND_GATV2>(a.H, a.D);
     else
         fn = dtype == GT_DTYPE_F32 ? pick_hd<float, KIND_GT>(a.H, a.D)
-             : (tu && tu->weights_fp32) ? pick_hd<bf16_tag, KIND_GT_WF32>(a.H, a.D)
+             : (tu && tu->bf16_weights) ? pick_hd<bf16_tag, KIND_GT_BF16W>(a.H, a.D)
                                         : pick_hd<bf16_tag, KIND_GT>(a.H, a.D);
     if (!fn)
         return fail(GT_ERROR_NOT_SUPPORTED, "unsupported (H, D) = (" + std::to_string(a.H) + ", " +

@@ -70,24 +70,23 @@ BF16_CASES = [(h, d) for (h, d, t) in CASES if t == "bf16"]
 
 @pytest.mark.parametrize("split", [False, True], ids=["default", "forced_split"])
 @pytest.mark.parametrize("H,D", BF16_CASES)
-def test_ragged_small_weights_fp32(H, D, split):
-    """bf16 features with the softmax weights kept in fp32 for P*V: the error
-    left is the bf16 rounding of the output (at most 2^-8 relative) plus
-    fp32 arithmetic, well inside the bf16 gate; the default rounds each
-    weight to bf16 as well (unit roundoff 2^-8), which adds up to 2^-8 of the
-    absolute sum."""
+def test_ragged_small_weight_precision(H, D, split):
+    """bf16 features: by default the softmax weights stay fp32 for P*V, so the
+    error left is the bf16 rounding of the output (unit roundoff 2^-8) plus
+    fp32 arithmetic, well inside the bf16 gate; the bf16_weights option rounds
+    each weight to bf16 as well, which adds up to 2^-8 of the absolute sum."""
     N = 300
     rowptr, colidx = synth.ragged_graph(H * 1000 + D + 5, N, max_deg=24, empty_frac=0.1,
                                         hubs={7: 299, 100: 150, 299: 70}, self_loops=True,
                                         dup_frac=0.05, shuffle=True)
     Q, K, V = synth.features(H * 1000 + D + 5, N, H, D, "bf16")
     scale = np.float32(1 / math.sqrt(D))
-    tuning = dict(FORCED_SPLIT if split else {}, weights_fp32=1)
-    got = run_gpu(rowptr, colidx, Q, K, V, scale, tuning=tuning)
+    base = FORCED_SPLIT if split else {}
     ref, absagg, _ = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale, want_lse=False)
+    got = run_gpu(rowptr, colidx, Q, K, V, scale, tuning=base or None)
     assert gate_error(got, ref, absagg) <= 2.0 ** -8 + 1e-5
-    dflt = run_gpu(rowptr, colidx, Q, K, V, scale, tuning=FORCED_SPLIT if split else None)
-    assert gate_error(dflt, ref, absagg) <= 2.0 ** -8 + 2.0 ** -8 + 1e-5
+    rounded = run_gpu(rowptr, colidx, Q, K, V, scale, tuning=dict(base, bf16_weights=1))
+    assert gate_error(rounded, ref, absagg) <= 2.0 ** -8 + 2.0 ** -8 + 1e-5
 
 
 @pytest.mark.parametrize("idx", [0, 1, 2, 3, 4, 5])

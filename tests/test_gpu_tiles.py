@@ -106,11 +106,13 @@ def test_tiles_ignored_for_fp32_and_wide_rows():
                                   tuning={"dense_tiles": 256}))
 
 
+@pytest.mark.parametrize("bf16_weights", [0, 1])
 @pytest.mark.parametrize("H,D", TILE_SHAPES)
-def test_tiles_weights_fp32(H, D):
-    """Tiles with fp32 weights (each weight as two bf16 terms, two P*V
-    products): only the bf16 output rounding (2^-8) and fp32-level terms are
-    left; lse to the fp32 tolerance."""
+def test_tiles_weight_precision(H, D, bf16_weights):
+    """Tiles keep each weight as two bf16 terms (two P*V products) by default:
+    only the bf16 output rounding (2^-8) and fp32-level terms are left; with
+    bf16_weights the rounded weights add up to 2^-8 of the absolute sum.  lse
+    to the fp32 tolerance either way (the normaliser sums the fp32 weights)."""
     import torch
     import paper_2605_31500_amd as gtm
     from tests.helpers import to_device
@@ -121,11 +123,11 @@ def test_tiles_weights_fp32(H, D):
     dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
     out = torch.empty_like(dev[2])
     lse = torch.empty((N, H), dtype=torch.float32, device=out.device)
-    gtm.gt_attn_fwd_ex(*dev, out, scale, tuning={"dense_tiles": 1, "weights_fp32": 1}, lse=lse)
+    gtm.gt_attn_fwd_ex(*dev, out, scale, tuning={"dense_tiles": 1, "bf16_weights": bf16_weights}, lse=lse)
     torch.cuda.synchronize()
     got = bf16_bits_to_f32(out.view(torch.int16).cpu().numpy().view(np.uint16))
     ref, absagg, ref_lse = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale)
-    assert gate_error(got, ref, absagg) <= 2.0 ** -8 + 1e-4
+    assert gate_error(got, ref, absagg) <= 2.0 ** -8 * (1 + bf16_weights) + 1e-4
     l = lse.cpu().numpy()
     fin = np.isfinite(ref_lse)
     assert np.array_equal(np.isneginf(l), ~fin)
