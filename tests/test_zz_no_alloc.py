@@ -98,3 +98,47 @@ def test_noalloc_calls_leave_device_memory_unchanged():
         gt.gt_attn_fwd_noalloc(*dev, out, 0.2)
     torch.cuda.synchronize()
     assert torch.cuda.mem_get_info()[0] == free0 and gt.gt_workspace_pool_stats() == pool0
+
+
+def test_noalloc_replays_in_a_hip_graph():
+    """The allocation-free entry point recorded into a HIP graph (torch's
+    graph capture on its capture stream) and replayed three times, with an
+    eager call of the same entry point on another graph between the replays
+    (it reuses the scratch array): every replay equals the eager result.  The
+    call records only kernels, no memset or allocation."""
+    import paper_2605_31500_amd as gt
+    H, D = 4, 32
+    rowptr, colidx = synth.ragged_graph(65, 30_000, max_deg=70, hubs={3: 29_999, 8: 9000}, self_loops=True)
+    Q, K, V = synth.features(65, 30_000, H, D, "bf16")
+    dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    out_eager = torch.empty_like(dev[2])
+    gt.gt_attn_fwd_noalloc(*dev, out_eager, 0.2)
+    torch.cuda.synchronize()
+    want = to_host_f32(out_eager)
+    rp2, ci2 = synth.ragged_graph(66, 5_000, max_deg=40, hubs={1: 4999}, self_loops=True)
+    Q2, K2, V2 = synth.features(66, 5_000, H, D, "bf16")
+    dev2 = [to_device(x) for x in (rp2, ci2, Q2, K2, V2)]
+    out2 = torch.empty_like(dev2[2])
+    gt.gt_attn_fwd_noalloc(*dev2, out2, 0.2)
+    torch.cuda.synchronize()
+    want2 = to_host_f32(out2)
+
+    out = torch.empty_like(dev[2])
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up on a side stream before capture, as torch asks
+        gt.gt_attn_fwd_noalloc(*dev, out, 0.2)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        gt.gt_attn_fwd_noalloc(*dev, out, 0.2)
+    for _ in range(3):
+        out.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host_f32(out), want)
+        out2.zero_()
+        gt.gt_attn_fwd_noalloc(*dev2, out2, 0.2)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host_f32(out2), want2)
