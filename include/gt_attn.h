@@ -64,9 +64,15 @@
 
 #ifdef __cplusplus
 extern "C" {
+/* In C++ the enumerations below have int as their fixed underlying type, so
+ * any int a C caller passes is a valid value there (and is refused by the
+ * argument checks) rather than an out-of-range enumeration value. */
+#define GT_ENUM_BASE : int
+#else
+#define GT_ENUM_BASE
 #endif
 
-typedef enum gt_status {
+typedef enum gt_status GT_ENUM_BASE {
     GT_SUCCESS = 0,
     GT_ERROR_INVALID_VALUE = 1, /* null pointer, bad size, misalignment, aliasing, non-finite scale */
     GT_ERROR_NOT_SUPPORTED = 2, /* (H, D) or dtype outside the compiled set */
@@ -74,7 +80,7 @@ typedef enum gt_status {
     GT_ERROR_HIP = 4            /* a HIP runtime call or kernel launch failed */
 } gt_status;
 
-typedef enum gt_dtype {
+typedef enum gt_dtype GT_ENUM_BASE {
     GT_DTYPE_F32 = 0,
     GT_DTYPE_BF16 = 1
 } gt_dtype;
@@ -266,7 +272,7 @@ gt_status gt_attn_bwd(gt_dtype dtype, const int64_t* rowptr, const int32_t* coli
  * dense_tiles is ignored.  Same ownership, workspace, asynchrony and error
  * contract as gt_attn_fwd.
  */
-typedef enum gt_reduce_op {
+typedef enum gt_reduce_op GT_ENUM_BASE {
     GT_REDUCE_MIN = 0,
     GT_REDUCE_MAX = 1
 } gt_reduce_op;
@@ -338,6 +344,8 @@ gt_status gt_workspace_pool_stats(int32_t device, uint64_t* reserved_bytes, uint
  * safe to call at any time from any thread.
  */
 gt_status gt_workspace_release(void);
+
+#undef GT_ENUM_BASE
 
 #ifdef __cplusplus
 }

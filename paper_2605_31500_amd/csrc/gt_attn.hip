@@ -1980,13 +1980,14 @@ gt_status run_bwd(gt_dtype dtype, const BwdArgs& a, hipStream_t stream) {
     if (!a.lse || reinterpret_cast<uintptr_t>(a.lse) % 4 != 0)
         return fail(GT_ERROR_INVALID_VALUE, "lse must be non-null and 4-byte aligned");
     const size_t bytes = (size_t)a.N * a.H * a.D * (dtype == GT_DTYPE_F32 ? 4 : 2);
-    for (const void* o : outs) {
+    for (int g = 0; g < 3; ++g) {
         for (const void* in : ins)
-            if (overlaps(o, bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "a gradient overlaps an input");
-        if (overlaps(o, bytes, a.lse, (size_t)a.N * a.H * sizeof(float)))
+            if (overlaps(outs[g], bytes, in, bytes)) return fail(GT_ERROR_INVALID_VALUE, "a gradient overlaps an input");
+        if (overlaps(outs[g], bytes, a.lse, (size_t)a.N * a.H * sizeof(float)))
             return fail(GT_ERROR_INVALID_VALUE, "a gradient overlaps lse");
-        for (const void* o2 : outs)
-            if (o2 != o && overlaps(o, bytes, o2, bytes)) return fail(GT_ERROR_INVALID_VALUE, "gradients overlap");
+        // distinct gradients, also when two are the same pointer
+        for (int g2 = g + 1; g2 < 3; ++g2)
+            if (overlaps(outs[g], bytes, outs[g2], bytes)) return fail(GT_ERROR_INVALID_VALUE, "gradients overlap");
     }
     return fn(a, stream);
 }

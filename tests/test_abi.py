@@ -205,6 +205,8 @@ def call_bwd(lib, dtype=0, rowptr=FAKE, colidx=FAKE, rowptr_t=FAKE, colidx_t=FAK
     (dict(dQ=0), 1), (dict(dK=FAKE + 0x700004), 1),            # gradient null / misaligned
     (dict(dQ=FAKE), 1),                                        # dQ aliases Q
     (dict(dV=FAKE + 0x700000 + 1024), 1),                      # dV overlaps dK
+    (dict(dK=FAKE + 0x600000), 1),                             # dK is dQ (same pointer)
+    (dict(dV=FAKE + 0x600000), 1),                             # dV is dQ
     (dict(dK=FAKE + 0x500000), 1),                             # dK overlaps lse
 ])
 def test_bwd_host_validation(lib, kw, status):
