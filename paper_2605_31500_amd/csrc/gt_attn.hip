@@ -842,17 +842,17 @@ gt_tile_kernel(TileParams p) {
     const int g16 = lane >> 4, n16 = lane & 15;  // MFMA lane coordinates
     // Workgroup b takes window b if the partition flagged it dense and returns
     // at once otherwise.  The count of dense windows (one word every
-    // workgroup reads) and the window's flag are loaded first and checked
-    // after the row-bound loads are issued, so a dense window waits on one
-    // round trip, and a graph without dense windows ends each workgroup on
-    // a cached word.  (A persistent loop over a list of the dense windows
-    // measured slower: it raised the kernel's register pressure past its
-    // 128-VGPR budget and spilled; a list also needs its entry before any
-    // other load.)
+    // workgroup reads, so a cached one) is loaded first: with none, the
+    // workgroup ends there; with every window dense, the window's own flag
+    // is not needed; otherwise it is read after the row-bound loads are
+    // issued.  (A persistent loop over a list of the dense windows measured
+    // slower: it raised the kernel's register pressure past its 128-VGPR
+    // budget and spilled; a list also needs its entry before any other load.)
     const int64_t r0 = (int64_t)blockIdx.x * kWin;
     const int64_t wend = r0 + kWin;
     const int32_t n_dense = CNT(p.counters, CNT_WIN);
-    const uint8_t flagged = p.win_flags[blockIdx.x];
+    if (n_dense == 0) return;
+    const bool all_dense = (int64_t)n_dense == (int64_t)gridDim.x;
 
     // bounds of this lane's row in the mask stage (4 lanes per row), loaded
     // first so that its entries can be requested right after the staging loads
@@ -864,7 +864,7 @@ gt_tile_kernel(TileParams p) {
         mb = p.rowptr[r];
         me = p.rowptr[r + 1];
     }
-    if (n_dense == 0 || !flagged) return;
+    if (!all_dense && !p.win_flags[blockIdx.x]) return;
 
     // ---- 1. staging
     if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];

@@ -70,6 +70,34 @@ def test_tiles_irregular(H, D):
     assert np.array_equal(a[64 * 9:64 * 10], csr[64 * 9:64 * 10])
 
 
+def test_tiles_window_flagged_but_below_threshold():
+    """The partition's density estimate samples every 8th light row of a
+    window.  Here the sampled rows point only inside their window and the
+    others only outside, so the window is flagged (estimate 1280 entries)
+    while it holds 160 in-window entries, below the threshold of 256: the
+    tile kernel must then stream all of its rows without a tile.  A second
+    window has the pattern reversed (estimate 0, 1120 in-window entries): it
+    stays on the CSR kernel, untiled."""
+    N = 64 * 3
+    rows = []
+    for i in range(N):
+        w = i // 64
+        inside = [64 * w + (i + 1 + t) % 64 for t in range(20)]
+        outside = [(64 * w + 64 + 3 * t + i) % N for t in range(20)]
+        outside = [j if j // 64 != w else (j + 64) % N for j in outside]
+        sampled = i % 8 == 0
+        if w == 0:
+            rows.append(sorted(inside if sampled else outside))
+        elif w == 1:
+            rows.append(sorted(outside if sampled else inside))
+        else:
+            rows.append(sorted(set(inside[:10] + outside[:10])))
+    rowptr, colidx = csr_from_rows(rows)
+    Q, K, V = synth.features(26, N, 2, 64, "bf16")
+    got = check(rowptr, colidx, Q, K, V, np.float32(0.125), tiles=256)
+    assert np.array_equal(got, run_gpu(rowptr, colidx, Q, K, V, np.float32(0.125)))  # the default
+
+
 def test_tiles_single_entry_exact():
     N, H, D = 64 * 8 + 5, 2, 64
     rowptr = np.arange(N + 1, dtype=np.int64)
