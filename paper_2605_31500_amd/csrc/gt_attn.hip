@@ -67,17 +67,23 @@ constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 constexpr int kXcds = 8;
 
-// Work-list counters in the workspace, cleared by a fill kernel at the start
-// of each call.  Each counter sits on its own 256-byte line so that atomics
-// on different counters do not serialise on one cache line.
 // Score kinds of the attention skeleton.
 // KIND_GT_BF16W: the graph-transformer score with each softmax weight rounded
 // to bf16 for P*V (bf16 rows pair two entries per dot2 instead of widening
 // their value rows); an option for rows whose steps are arithmetic-bound.
 enum { KIND_GT = 0, KIND_GATV2 = 1, KIND_GT_BF16W = 2 };
 
-// CNT_LIGHT: light rows left in the light-row order (shapes that build one);
-// CNT_WIN: dense-tile windows flagged by the partition.
+// Work-list counters in the workspace, cleared by a fill kernel at the start
+// of each call.  Each counter sits on its own 256-byte line so that atomics
+// on different counters do not serialise on one cache line.
+//   CNT_MED, CNT_HEAVY, CNT_CHUNKS, CNT_SLOTS: medium rows, split rows, work
+//     items, partial slots (list lengths, reserved with atomics);
+//   CNT_OVERFLOW: set if a list capacity was exceeded (the CSR precondition
+//     was violated; the excess entries are dropped);
+//   CNT_LIGHT: nonzero if the light-row order holds any row (shapes that build
+//     one); a flag written with plain stores;
+//   CNT_WIN: byte 0 nonzero if some window was found dense, byte 1 if some
+//     window was not (byte flags written with plain stores, read as one word).
 enum {
     CNT_MED = 0, CNT_HEAVY = 1, CNT_CHUNKS = 2, CNT_OVERFLOW = 3, CNT_SLOTS = 4, CNT_LIGHT = 5, CNT_WIN = 6,
     CNT_COUNT = 7
@@ -737,10 +743,10 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
 // neighbourhoods into tiles for matrix cores; this is a gfx950 design of the
 // same idea, not the paper's 16x8 TCB format).  Rows are grouped in aligned
 // windows of 64; the window's own 64 ids are its tile columns.  The partition
-// kernel lists the windows whose light rows it estimates to be dense (a
+// kernel flags the windows whose light rows it estimates to be dense (a
 // sample of one entry in every 8th light row); this kernel takes every light
-// row of a listed window (a workgroup per window, looping over the list),
-// the CSR kernel every other row:
+// row of a flagged window (one workgroup per window), the CSR kernel every
+// other row:
 //   1. stage the window's rowptr, its K rows and its V rows (transposed) in
 //      LDS with independent loads, and each light row's entries in registers;
 //   2. per light row, a 64-bit mask of its in-window entries (a row with a
@@ -786,7 +792,7 @@ struct TileParams {
     int32_t light_max;  // <= kWinMaxDeg
     int32_t min_entries;
     const uint8_t* win_flags;  // [ceil(N / 64)]: 1 for the dense windows the partition found
-    const int32_t* counters;   // CNT_WIN: how many there are
+    const int32_t* counters;   // CNT_WIN: any window dense (byte 0) / not dense (byte 1)
 };
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
@@ -841,18 +847,18 @@ gt_tile_kernel(TileParams p) {
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
     const int g16 = lane >> 4, n16 = lane & 15;  // MFMA lane coordinates
     // Workgroup b takes window b if the partition flagged it dense and returns
-    // at once otherwise.  The count of dense windows (one word every
-    // workgroup reads, so a cached one) is loaded first: with none, the
-    // workgroup ends there; with every window dense, the window's own flag
-    // is not needed; otherwise it is read after the row-bound loads are
-    // issued.  (A persistent loop over a list of the dense windows measured
-    // slower: it raised the kernel's register pressure past its 128-VGPR
-    // budget and spilled; a list also needs its entry before any other load.)
+    // at once otherwise.  The word of window flags (one word every workgroup
+    // reads, so a cached one) is loaded first: with no dense window, the
+    // workgroup ends there; with no sparse one, the window's own flag is not
+    // needed; otherwise it is read after the row-bound loads are issued.  (A
+    // persistent loop over a list of the dense windows measured slower: it
+    // raised the kernel's register pressure past its 128-VGPR budget and
+    // spilled; a list also needs its entry before any other load.)
     const int64_t r0 = (int64_t)blockIdx.x * kWin;
     const int64_t wend = r0 + kWin;
-    const int32_t n_dense = CNT(p.counters, CNT_WIN);
-    if (n_dense == 0) return;
-    const bool all_dense = (int64_t)n_dense == (int64_t)gridDim.x;
+    const int32_t win_state = CNT(p.counters, CNT_WIN);
+    if ((win_state & 0xFF) == 0) return;
+    const bool all_dense = (win_state & 0xFF00) == 0;
 
     // bounds of this lane's row in the mask stage (4 lanes per row), loaded
     // first so that its entries can be requested right after the staging loads
@@ -1226,8 +1232,9 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
             tiled[k] = dense && lt;
             const int64_t win = (r0 + k * kBlock + wv * kWave) >> 6;
             if (lane == 0) {
-                if (win * kWave < p.N) p.win_flags[win] = dense ? 1 : 0;
-                win_dense[k][wv] = dense ? 1 : 0;
+                const bool exists = win * kWave < p.N;
+                if (exists) p.win_flags[win] = dense ? 1 : 0;
+                win_dense[k][wv] = !exists ? 2 : dense ? 1 : 0;  // 2: past the last row
             }
         }
     }
@@ -1275,30 +1282,32 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     int tots[3];
     const int3 offs = block_exclusive_scan3(make_int3(n_heavy, n_chunk, n_slot), scan3, tots);
     const int off_h = offs.x, off_c = offs.y, off_s = offs.z;
-    // The block's reservations: lanes 0..5 of wave 0 each add to one counter,
-    // so the atomics go out together rather than one after another.
-    if (threadIdx.x < 6) {
+    // The block's reservations: lanes 0..3 of wave 0 each add to one list
+    // counter, so the atomics go out together rather than one after another;
+    // lanes 4..6 raise flags with plain stores.
+    if (threadIdx.x < 7) {
         const int t = threadIdx.x;
-        int amount = 0, which = CNT_MED;
-        if (t == 0) {
-            for (int k = 0; k < kPartRowsPerThread; ++k)
-                for (int w = 0; w < kWavesPerBlock; ++w) amount += wave_cnt[k][w];
-        } else if (t < 4) {
-            amount = tots[t - 1];
-            which = t == 1 ? CNT_HEAVY : t == 2 ? CNT_CHUNKS : CNT_SLOTS;
-        } else if (t == 4) {
-            // light rows left in the order: zero lets the attention kernel
-            // skip its light-row loop (every light row in dense windows)
-            amount = p.light_list ? cls_cnt[0] : 0;
-            which = CNT_LIGHT;
-        } else {
-            if (p.win_flags)
+        if (t < 4) {
+            int amount = 0, which = CNT_MED;
+            if (t == 0) {
                 for (int k = 0; k < kPartRowsPerThread; ++k)
-                    for (int w = 0; w < kWavesPerBlock; ++w) amount += win_dense[k][w];
-            which = CNT_WIN;
+                    for (int w = 0; w < kWavesPerBlock; ++w) amount += wave_cnt[k][w];
+            } else {
+                amount = tots[t - 1];
+                which = t == 1 ? CNT_HEAVY : t == 2 ? CNT_CHUNKS : CNT_SLOTS;
+            }
+            base[t] = amount ? atomicAdd(&CNT(p.counters, which), amount) : 0;
+        } else if (t == 4) {
+            // light rows left in the order: none lets the attention kernel
+            // skip its light-row loop (every light row in dense windows)
+            if (p.light_list && cls_cnt[0] > 0) CNT(p.counters, CNT_LIGHT) = 1;
+        } else if (p.win_flags) {
+            const int want = t == 5 ? 1 : 0;  // lane 5: a dense window; lane 6: a sparse one
+            bool seen = false;
+            for (int k = 0; k < kPartRowsPerThread; ++k)
+                for (int w = 0; w < kWavesPerBlock; ++w) seen |= win_dense[k][w] == want;
+            if (seen) reinterpret_cast<uint8_t*>(&CNT(p.counters, CNT_WIN))[t - 5] = 1;
         }
-        const int b = amount ? atomicAdd(&CNT(p.counters, which), amount) : 0;
-        if (t < 4) base[t] = b;
     }
     __syncthreads();
     int pos = base[0];
@@ -1341,11 +1350,10 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     }
 }
 
-// Launches the degree binning over pp.N rows.  The blocks' list reservations
-// (one atomic per list and block) serialise on the list counters, so large
-// graphs take 2048 rows per block; smaller ones take 1024, giving more blocks
-// in parallel.  Measured on MI355X: 169K rows 12.8 -> 10.5 us with 1024;
-// 2.1M rows 32 -> 44 us with 1024.
+// Launches the degree binning over pp.N rows.  Large graphs take 2048 rows
+// per block, smaller ones 1024, giving more blocks in parallel.  Measured on
+// MI355X: 169K rows 12.8 -> 10.5 us with 1024; 2.1M rows 32 -> 44 us with
+// 1024.
 hipError_t launch_partition(const PartParams& pp, hipStream_t stream) {
     if (pp.N <= (int64_t(1) << 19)) {
         const int grid = (int)((pp.N + 4 * kBlock - 1) / (4 * kBlock));
