@@ -388,6 +388,23 @@ struct RowState {
         }
     }
 
+    // begin() with this lane's 16-byte pieces of the row vector already in
+    // registers (graph-transformer score only).
+    __device__ __forceinline__ void begin_loaded(const uint4 (&r)[Gm::kNV]) {
+        static_assert(!kGat, "the GATv2 state also needs its attention vector");
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            if constexpr (kDot2)
+                qraw[k] = r[k];
+            else
+                widen<T>(r[k], q[k]);
+            m[k] = -INFINITY;
+            l[k] = 0.0f;
+#pragma unroll
+            for (int e = 0; e < Gm::kEPV; ++e) acc[k][e] = 0.0f;
+        }
+    }
+
     // Loads of one step: the K and V rows (GATv2: the R rows) of U entries,
     // 16 bytes per lane each.
     struct Batch {
@@ -825,6 +842,16 @@ struct TileLds {
 
 // Four workgroups per CU fit the LDS of a window (about 40 KB) when H*D <= 128
 // and H <= 2; those shapes are held to 128 VGPRs so that registers allow it too.
+// The stream stage of the tile kernel takes the row vectors of its rows from
+// the strip's MFMA operand registers by cross-lane moves instead of reading Q
+// a second time (on the SBM workload: 268 MB less fetched, about 10 us per
+// call); for the 1x128 fp32-weight shape that holds 16 more registers across
+// the products and spills, so it reads Q again.
+template <int H, int D, int KIND>
+struct QFromOperands {
+    static constexpr bool value = !(H == 1 && D == 128 && KIND == KIND_GT);
+};
+
 template <int H, int D>
 struct TileWaves {
     static constexpr int value = H <= 2 ? 4 : 1;
@@ -1048,6 +1075,26 @@ gt_tile_kernel(TileParams p) {
     int32_t* gtile = lds.big.rest.ctile[wv] + g * kWinMaxDeg;
     constexpr int kRowPer = (kWinMaxDeg + G - 1) / G;  // a light row: at most kWinMaxDeg entries
     constexpr int kPasses = 16 / P;
+    // The row vectors of the group's rows, from the strip's MFMA operands
+    // (lane 16*g16 + n16 of qreg[t] holds elements 32t + 8*g16 .. + 7 of strip
+    // row n16) by cross-lane moves, rather than a second read from memory.
+    constexpr bool kQRegs = QFromOperands<H, D, KIND>::value;
+    uint4 qpass[kQRegs ? kPasses : 1][Gm::kNV];
+#pragma unroll
+    for (int pass = 0; pass < (kQRegs ? kPasses : 0); ++pass)
+#pragma unroll
+        for (int k = 0; k < Gm::kNV; ++k) {
+            const int e0 = 8 * (lig + k * G);  // first element of this lane's piece
+            const int src = 16 * ((e0 % 32) / 8) + pass * P + g;
+            uint4 v = make_uint4(0, 0, 0, 0);
+#pragma unroll
+            for (int t = 0; t < HD / 32; ++t) {
+                const uint4 x = make_uint4(__shfl((int)qreg[t].x, src), __shfl((int)qreg[t].y, src),
+                                           __shfl((int)qreg[t].z, src), __shfl((int)qreg[t].w, src));
+                if (t == e0 / 32) v = x;
+            }
+            qpass[pass][k] = v;
+        }
     auto load_entries = [&](int pass, int32_t (&e)[kRowPer]) {
         const int sr = pass * P + g, wr = 16 * wv + sr;
         const int64_t eb = lds.rp[wr], ee = lds.rp[wr + 1];
@@ -1072,7 +1119,10 @@ gt_tile_kernel(TileParams p) {
         const int wr = 16 * wv + sr;
         const int64_t row = r0 + wr;
         RS st;
-        st.begin(p.Q, row, lig);
+        if constexpr (kQRegs)
+            st.begin_loaded(qpass[pass]);
+        else
+            st.begin(p.Q, row, lig);
         if (use_tile) {
 #pragma unroll
             for (int k = 0; k < Gm::kNV; ++k) {
