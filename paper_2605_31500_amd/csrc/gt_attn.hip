@@ -728,9 +728,12 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     int32_t* tile = tiles[wv];
 
     // Counts come from the partition kernel; clamping keeps every list read
-    // inside the workspace even if the CSR precondition were violated.
+    // inside the workspace even if the CSR precondition were violated.  The
+    // light-row flag is read with them, so that a workgroup with nothing to
+    // do ends after one round trip.
     const int32_t n_chunks = min(CNT(p.counters, CNT_CHUNKS), p.cap_items);
     const int32_t n_items = n_chunks + (int32_t)min((int64_t)CNT(p.counters, CNT_MED), p.N);
+    const bool any_light = !SortedLight<T, H, D, KIND>::value || CNT(p.counters, CNT_LIGHT) != 0;
     const int nwaves = gridDim.x * kWavesPerBlock;
     for (int it = blockIdx.x * kWavesPerBlock + wv; it < n_items; it += nwaves) {
         if (it < n_chunks) {
@@ -748,9 +751,9 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
     const int64_t n_light = (p.N + Gm::kP - 1) / Gm::kP;
     const int64_t lo = n_light * xcd / kXcds, hi = n_light * (xcd + 1) / kXcds;
     const int g = lane / Gm::kG, lig = lane % Gm::kG;
-    // (with a light-row order, its count can be zero: every light row lies in
-    // a dense window of the tile kernel)
-    if (SortedLight<T, H, D, KIND>::value && CNT(p.counters, CNT_LIGHT) == 0) return;
+    // (with a light-row order, it can be empty: every light row lies in a
+    // dense window of the tile kernel)
+    if (!any_light) return;
     light_rows<T, H, D, KIND>(p, lo + lw, hi, waves_per_xcd, g, lig, tile + g * LightTile<Gm::kG>::kEntries);
 }
 
