@@ -34,13 +34,18 @@
  * `out` must not overlap Q, K or V.  Q, K, V and out must be 16-byte aligned.
  * Workspace (degree-bin lists, the light-row order of narrow-row shapes,
  * partial softmax states of split rows and the work-list counters) is owned
- * by the library and private to each call: it is allocated from the
- * library's memory pool of the device with hipMallocFromPoolAsync on
- * `stream` and freed with hipFreeAsync on `stream` after the call's kernels,
- * so calls on different streams (or host threads) never share it and nothing
- * is cached per stream.  The pool keeps up to 256 MiB of freed workspace
- * across synchronisations for reuse; gt_workspace_release() returns it to
- * the device.
+ * by the library and private to each call while its kernels run: a call
+ * takes a free workspace block of the device and, after enqueueing its
+ * kernels, hands it back tagged with an event recorded on `stream`.  A later
+ * call (any stream, any host thread) reuses a free block only once that
+ * event has completed, or, for a block last used on its own stream, behind a
+ * device-side wait on the event; otherwise it allocates a new block from the
+ * library's memory pool of the device (hipMallocFromPoolAsync on `stream`).
+ * The host never waits for the device, nothing is kept per stream, and free
+ * blocks above 256 MiB per device go back to the pool; gt_workspace_release()
+ * returns all free blocks to the device.  On a stream being captured into a
+ * graph the workspace is allocated and freed stream-ordered instead (both
+ * become graph nodes).
  *
  * Semantics: asynchronous.  GT_SUCCESS means the work was enqueued on
  * `stream`; device faults surface at the caller's next synchronisation.
@@ -331,17 +336,21 @@ gt_status gt_profile_enable(int32_t enable);
 gt_status gt_profile_collect(double ms[3], int64_t* calls);
 
 /*
- * Memory of the library's workspace pool on `device` (host outputs): bytes
- * the pool holds from the device, and bytes of it in use by calls whose
- * workspace is not yet freed in stream order.  Both 0 before the device's
- * first call.
+ * Memory of the library's workspace on `device` (host outputs): bytes the
+ * pool holds from the device (free blocks kept for reuse included), and bytes
+ * of workspace blocks held by calls still being enqueued on the host (0 when
+ * no call is in progress; a returned call's block is free for reuse once its
+ * kernels are done).  Both 0 before the device's first call.
  */
 gt_status gt_workspace_pool_stats(int32_t device, uint64_t* reserved_bytes, uint64_t* used_bytes);
 
 /*
- * Returns the unused memory of the library's workspace pools to the devices
- * (hipMemPoolTrimTo).  Workspace of calls still in flight is not affected;
- * safe to call at any time from any thread.
+ * Returns the free workspace blocks and the unused memory of the library's
+ * workspace pools to the devices: waits for each free block's last use
+ * (hipEventSynchronize), frees it, then trims the pool (hipMemPoolTrimTo).
+ * Blocks held by calls in progress are not affected; safe to call at any time
+ * from any thread.  Blocking: it waits for the device work that last used a
+ * free block.
  */
 gt_status gt_workspace_release(void);
 

@@ -1555,16 +1555,29 @@ struct PhaseEvents {
     }
 };
 
-// Workspace.  Every call takes its own workspace (degree-bin lists, partial
-// states of split rows, work-list counters) from the library's memory pool of
-// the device, allocated and freed stream-ordered on the call's stream
-// (hipMallocFromPoolAsync / hipFreeAsync): calls on different streams never
-// share memory, and nothing is keyed by stream or pointer.  The pool keeps up
-// to kPoolKeepBytes of freed memory across synchronisations for reuse, so a
-// steady sequence of calls does not go back to the device allocator;
-// gt_workspace_release() returns the rest.
+// Workspace.  Every call takes a workspace block (degree-bin lists, partial
+// states of split rows, work-list counters) for its own use and hands it back
+// once its kernels are enqueued; the block is then tagged with an event
+// recorded on the call's stream after those kernels.  A later call, on any
+// stream, takes a free block only if its event has completed, or if it was
+// last used on the same stream, and then with a device-side wait on the event
+// (hipStreamWaitEvent: stream order already implies it, and it keeps a
+// recycled stream handle safe); the host never waits.  Otherwise the call
+// gets a new block from the library's memory pool of the device
+// (hipMallocFromPoolAsync on its stream).  Blocks are not tied to streams or
+// pointers, and free blocks beyond kCacheBytes per device go back to the pool
+// (stream-ordered after their last use); gt_workspace_release() returns every
+// free block and trims the pools.  (Freeing each call's block with
+// hipFreeAsync made the host wait in every call for the previous call's
+// kernels, about 485 us per call behind a 0.5 ms kernel, so the host could
+// never run ahead of the device.)  While the call's stream is being captured
+// into a graph, the block is allocated and freed stream-ordered instead (both
+// become graph nodes), since events recorded during a capture cannot be
+// queried.
 constexpr int kMaxDevices = 64;
 constexpr uint64_t kPoolKeepBytes = uint64_t(256) << 20;
+constexpr size_t kCacheBytes = size_t(256) << 20;  // free blocks kept per device
+constexpr size_t kBlockGranule = size_t(1) << 20;
 
 struct DevicePools {
     std::once_flag once[kMaxDevices];
@@ -1601,17 +1614,88 @@ hipError_t pool_of(int dev, hipMemPool_t* out) {
     return dp.err[dev];
 }
 
-// One call's workspace; freed stream-ordered after the call's kernels when it
-// goes out of scope (also on an error return after some launches).
+struct WsBlock {
+    char* ptr = nullptr;
+    size_t bytes = 0;
+    hipEvent_t ev = nullptr;       // recorded after the last user's kernels
+    hipStream_t last = nullptr;    // the last user's stream
+};
+
+// Free blocks of one device, and the bytes of blocks that calls hold.
+struct BlockCache {
+    std::mutex mu;
+    std::vector<WsBlock> free_blocks;
+    size_t free_bytes = 0;
+    size_t taken_bytes = 0;
+};
+BlockCache& block_cache(int dev) {
+    static BlockCache* c = new BlockCache[kMaxDevices];
+    return c[dev];
+}
+
+// Returns a block to the pool after its last use: ordered after the block's
+// event on `stream` (the stream of the call that lets it go).
+void free_block(const WsBlock& b, hipStream_t stream) {
+    if (b.ev) {
+        if (hipEventQuery(b.ev) != hipSuccess) (void)hipStreamWaitEvent(stream, b.ev, 0);
+        (void)hipGetLastError();
+        (void)hipEventDestroy(b.ev);
+    }
+    (void)hipFreeAsync(b.ptr, stream);
+}
+
+// One call's workspace; handed back (cached) or freed stream-ordered after
+// the call's kernels when it goes out of scope (also on an error return
+// after some launches).
 struct CallWorkspace {
+    enum Kind { NONE, CACHED, STREAM_ORDERED, SCRATCH };
     char* ptr = nullptr;
     hipStream_t stream = nullptr;
-    bool pooled = false;
+    int dev = -1;
+    Kind kind = NONE;
+    WsBlock block;
     CallWorkspace() = default;
     CallWorkspace(const CallWorkspace&) = delete;
     CallWorkspace& operator=(const CallWorkspace&) = delete;
     ~CallWorkspace() {
-        if (pooled && ptr) (void)hipFreeAsync(ptr, stream);
+        if (kind == STREAM_ORDERED) {
+            (void)hipFreeAsync(ptr, stream);
+        } else if (kind == CACHED) {
+            BlockCache& c = block_cache(dev);
+            if (hipEventRecord(block.ev, stream) != hipSuccess) {
+                // no event, no safe reuse: free it in stream order
+                (void)hipGetLastError();
+                (void)hipEventDestroy(block.ev);
+                block.ev = nullptr;
+                (void)hipFreeAsync(block.ptr, stream);
+                std::lock_guard<std::mutex> lk(c.mu);
+                c.taken_bytes -= block.bytes;
+                return;
+            }
+            block.last = stream;
+            std::vector<WsBlock> evict;
+            {
+                std::lock_guard<std::mutex> lk(c.mu);
+                c.taken_bytes -= block.bytes;
+                c.free_blocks.push_back(block);
+                c.free_bytes += block.bytes;
+                // over the cache bound: give back free blocks, completed ones
+                // first, then the oldest
+                while (c.free_bytes > kCacheBytes && !c.free_blocks.empty()) {
+                    size_t k = 0;
+                    for (size_t i = 0; i < c.free_blocks.size(); ++i)
+                        if (hipEventQuery(c.free_blocks[i].ev) == hipSuccess) {
+                            k = i;
+                            break;
+                        }
+                    c.free_bytes -= c.free_blocks[k].bytes;
+                    evict.push_back(c.free_blocks[k]);
+                    c.free_blocks.erase(c.free_blocks.begin() + (std::ptrdiff_t)k);
+                }
+            }
+            (void)hipGetLastError();
+            for (const WsBlock& b : evict) free_block(b, stream);
+        }
     }
 };
 
@@ -1620,13 +1704,69 @@ gt_status acquire_workspace(int dev, size_t bytes, hipStream_t stream, CallWorks
     hipError_t he = pool_of(dev, &pool);
     if (he != hipSuccess) return hip_fail(he, "workspace pool");
     ws.stream = stream;
-    he = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws.ptr), bytes, pool, stream);
-    if (he != hipSuccess || !ws.ptr) {
+    ws.dev = dev;
+    const size_t need = (bytes + kBlockGranule - 1) / kBlockGranule * kBlockGranule;
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if ((he = hipStreamIsCapturing(stream, &cap)) != hipSuccess) return hip_fail(he, "hipStreamIsCapturing");
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (!capturing) {
+        // a free block that fits: completed first, then last used on this
+        // stream; the smallest such
+        BlockCache& c = block_cache(dev);
+        bool found = false, done = false;
+        {
+            std::lock_guard<std::mutex> lk(c.mu);
+            size_t best = 0;
+            int best_rank = 2;
+            for (size_t i = 0; i < c.free_blocks.size(); ++i) {
+                const WsBlock& b = c.free_blocks[i];
+                if (b.bytes < need) continue;
+                const hipError_t q = hipEventQuery(b.ev);
+                const int rank = q == hipSuccess ? 0 : (q == hipErrorNotReady && b.last == stream) ? 1 : 2;
+                if (rank < best_rank || (rank == best_rank && rank < 2 && b.bytes < c.free_blocks[best].bytes)) {
+                    best = i;
+                    best_rank = rank;
+                }
+            }
+            (void)hipGetLastError();  // a query's not-ready status
+            if (best_rank < 2) {
+                ws.block = c.free_blocks[best];
+                c.free_blocks.erase(c.free_blocks.begin() + (std::ptrdiff_t)best);
+                c.free_bytes -= ws.block.bytes;
+                c.taken_bytes += ws.block.bytes;
+                found = true;
+                done = best_rank == 0;
+            }
+        }
+        if (found) {
+            ws.kind = CallWorkspace::CACHED;
+            ws.ptr = ws.block.ptr;
+            if (!done && (he = hipStreamWaitEvent(stream, ws.block.ev, 0)) != hipSuccess)
+                return hip_fail(he, "workspace wait");
+            return GT_SUCCESS;
+        }
+    }
+    void* p = nullptr;
+    he = hipMallocFromPoolAsync(&p, capturing ? bytes : need, pool, stream);
+    if (he != hipSuccess || !p) {
         (void)hipGetLastError();
-        ws.ptr = nullptr;
         return fail(GT_ERROR_OUT_OF_MEMORY, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
     }
-    ws.pooled = true;
+    ws.ptr = static_cast<char*>(p);
+    if (capturing) {
+        ws.kind = CallWorkspace::STREAM_ORDERED;
+        return GT_SUCCESS;
+    }
+    hipEvent_t ev = nullptr;
+    if ((he = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) {
+        ws.kind = CallWorkspace::STREAM_ORDERED;  // freed in stream order on return
+        return hip_fail(he, "workspace event");
+    }
+    ws.block = WsBlock{ws.ptr, need, ev, stream};
+    ws.kind = CallWorkspace::CACHED;
+    BlockCache& c = block_cache(dev);
+    std::lock_guard<std::mutex> lk(c.mu);
+    c.taken_bytes += need;
     return GT_SUCCESS;
 }
 
@@ -1668,7 +1808,7 @@ gt_status call_workspace(bool noalloc, int dev, size_t bytes, hipStream_t stream
     if (he != hipSuccess) return hip_fail(he, "hipGetSymbolAddress(scratch)");
     ws.ptr = p;
     ws.stream = stream;
-    ws.pooled = false;
+    ws.kind = CallWorkspace::SCRATCH;
     return GT_SUCCESS;
 }
 
@@ -2259,12 +2399,13 @@ gt_status gt_workspace_pool_stats(int32_t device, uint64_t* reserved_bytes, uint
     if (device < 0 || device >= kMaxDevices) return fail(GT_ERROR_INVALID_VALUE, "device out of range");
     DevicePools& dp = device_pools();
     if (!dp.ready[device].load(std::memory_order_acquire) || !dp.pool[device]) return GT_SUCCESS;
-    uint64_t r = 0, u = 0;
-    hipError_t he = hipMemPoolGetAttribute(dp.pool[device], hipMemPoolAttrReservedMemCurrent, &r);
-    if (he == hipSuccess) he = hipMemPoolGetAttribute(dp.pool[device], hipMemPoolAttrUsedMemCurrent, &u);
+    uint64_t r = 0;
+    const hipError_t he = hipMemPoolGetAttribute(dp.pool[device], hipMemPoolAttrReservedMemCurrent, &r);
     if (he != hipSuccess) return hip_fail(he, "hipMemPoolGetAttribute");
+    BlockCache& c = block_cache(device);
+    std::lock_guard<std::mutex> lk(c.mu);
     *reserved_bytes = r;
-    *used_bytes = u;
+    *used_bytes = c.taken_bytes;
     return GT_SUCCESS;
 }
 
@@ -2272,15 +2413,33 @@ gt_status gt_workspace_release(void) {
     t_last_error.clear();
     DevicePools& dp = device_pools();
     gt_status st = GT_SUCCESS;
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) cur = -1;
     for (int dev = 0; dev < kMaxDevices; ++dev) {
         // a device's pool is created by its first call; devices without one
         // are skipped
         if (!dp.ready[dev].load(std::memory_order_acquire)) continue;
         hipMemPool_t pool = dp.pool[dev];
         if (!pool) continue;
-        const hipError_t he = hipMemPoolTrimTo(pool, 0);
-        if (he != hipSuccess) st = hip_fail(he, "trimming a workspace pool");
+        std::vector<WsBlock> blocks;
+        {
+            BlockCache& c = block_cache(dev);
+            std::lock_guard<std::mutex> lk(c.mu);
+            blocks.swap(c.free_blocks);
+            c.free_bytes = 0;
+        }
+        hipError_t he = hipSetDevice(dev);
+        // each free block after its last use, then the pool down to nothing
+        for (const WsBlock& b : blocks) {
+            if (he == hipSuccess) he = hipEventSynchronize(b.ev);
+            (void)hipEventDestroy(b.ev);
+            if (he == hipSuccess) he = hipFreeAsync(b.ptr, nullptr);
+        }
+        if (he == hipSuccess) he = hipStreamSynchronize(nullptr);
+        if (he == hipSuccess) he = hipMemPoolTrimTo(pool, 0);
+        if (he != hipSuccess) st = hip_fail(he, "returning workspace of a device");
     }
+    if (cur >= 0) (void)hipSetDevice(cur);
     return st;
 }
 

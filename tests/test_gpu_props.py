@@ -361,6 +361,71 @@ def test_workspace_reuse_growth_and_release():
     assert gate_error(b1, ref, absagg) <= TOL_F32
 
 
+def test_calls_return_without_waiting_for_the_device():
+    """A call enqueues its work and returns: behind a device-side sleep on its
+    stream, five calls take a small fraction of the sleep on the host (freeing
+    each call's workspace stream-ordered made every call wait for the previous
+    call's kernels), and all five results are right."""
+    import time
+    import paper_2605_31500_amd as gtm
+    N, H, D = 60_000, 4, 32
+    rowptr, colidx = synth.chung_lu_graph(21, N)
+    Q, K, V = synth.features(21, N, H, D, "f32")
+    want = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.2))
+    dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    outs = [torch.empty_like(dev[2]) for _ in range(5)]
+    gtm.gt_attn_fwd(*dev, outs[0], np.float32(0.2))  # a free block whose work is done
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    torch.cuda._sleep(int(2e8))  # 2e8 shader clock cycles: about 0.1 s
+    t1 = time.perf_counter()
+    for o in outs:
+        gtm.gt_attn_fwd(*dev, o, np.float32(0.2))
+    host = time.perf_counter() - t1
+    torch.cuda.current_stream().synchronize()
+    total = time.perf_counter() - t0
+    print("five calls behind a %.3f s device sleep: %.4f s on the host" % (total, host), flush=True)
+    assert total > 0.02
+    assert host < 0.25 * total, "calls waited for the device: %.4f of %.4f s" % (host, total)
+    for o in outs:
+        assert np.array_equal(to_host_f32(o), want)
+
+
+def test_block_in_use_on_another_stream_is_not_handed_out():
+    """A workspace block whose last call is still pending on stream A is not
+    given to a call on stream B: B's call gets a block of its own (the pool
+    grows), and both results are right."""
+    import paper_2605_31500_amd as gtm
+    N, H, D = 60_000, 4, 32
+    rowptr, colidx = synth.chung_lu_graph(22, N)
+    Qa, Ka, Va = synth.features(22, N, H, D, "f32")
+    Qb, Kb, Vb = synth.features(23, N, H, D, "f32")
+    want_a = run_gpu(rowptr, colidx, Qa, Ka, Va, np.float32(0.2))
+    want_b = run_gpu(rowptr, colidx, Qb, Kb, Vb, np.float32(0.2))
+    rp, ci = to_device(rowptr), to_device(colidx)
+    fa = [to_device(x) for x in (Qa, Ka, Va)]
+    fb = [to_device(x) for x in (Qb, Kb, Vb)]
+    out_a, out_b = torch.empty_like(fa[0]), torch.empty_like(fb[0])
+    torch.cuda.synchronize()
+    gtm.gt_workspace_release()
+    gtm.gt_attn_fwd(rp, ci, *fa, out_a, np.float32(0.2))  # one block, done after the sync
+    torch.cuda.synchronize()
+    one_block = gtm.gt_workspace_pool_stats()[0]
+    assert one_block > 0
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(sa):
+        torch.cuda._sleep(int(2e8))
+        gtm.gt_attn_fwd(rp, ci, *fa, out_a, np.float32(0.2), stream=sa)
+    with torch.cuda.stream(sb):
+        gtm.gt_attn_fwd(rp, ci, *fb, out_b, np.float32(0.2), stream=sb)
+    grown = gtm.gt_workspace_pool_stats()[0]
+    sa.synchronize()
+    sb.synchronize()
+    assert grown > one_block, "stream B took the block still pending on stream A"
+    assert np.array_equal(to_host_f32(out_a), want_a)
+    assert np.array_equal(to_host_f32(out_b), want_b)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("tuning", [None, "group_per_row", "small_light"])
 def test_step_ordered_light_rows(dtype, tuning):
@@ -419,12 +484,13 @@ def test_small_graph_short_chunks(kind, N):
 
 
 def test_workspace_memory_comes_back_after_many_streams():
-    """Calls on 50 streams created and dropped one after another: workspace is
-    per call (pooled, stream-ordered), so the memory the library's pool holds
-    afterwards is bounded by its 256 MiB reuse threshold, not 50 workspaces;
-    none of it is in use once the calls are done, and gt_workspace_release()
-    returns all of it to the device.  Each call's workspace here is about
-    40 MB (short chunks give many partial states)."""
+    """Calls on 50 streams created and dropped one after another: workspace
+    blocks are not kept per stream (a block whose last use is done serves the
+    next call on any stream), so the memory the library holds afterwards is
+    bounded by its 256 MiB cache, not 50 workspaces; no block is held once
+    the calls are done, and gt_workspace_release() returns all of it to the
+    device.  Each call's workspace here is about 40 MB (short chunks give
+    many partial states)."""
     import paper_2605_31500_amd as gtm
     N, H, D = 200_000, 4, 32
     rowptr, colidx = synth.chung_lu_graph(3, N)
