@@ -174,6 +174,9 @@ struct PartParams {
     const int32_t* colidx = nullptr;
     uint8_t* win_flags = nullptr;  // [ceil(N / 64)]
     int32_t tile_min = 0;
+    // the workspace's other counter set, zeroed by block 0 for the next call
+    // that takes this workspace (nullptr: none)
+    int32_t* zero_next = nullptr;
 };
 
 struct MergeParams {
@@ -1226,6 +1229,8 @@ __global__ void __launch_bounds__(kBlock) gt_partition_kernel(PartParams p) {
     bool med[kPartRowsPerThread];
     uint64_t mask[kPartRowsPerThread];
     int n_heavy = 0, n_chunk = 0, n_slot = 0;
+    if (p.zero_next && blockIdx.x == 0)
+        for (int i = threadIdx.x; i < kCntSetWords; i += kBlock) p.zero_next[i] = 0;
     if (p.light_list && threadIdx.x < kLightClasses) cls_cnt[threadIdx.x] = 0;
 #pragma unroll
     for (int k = 0; k < kPartRowsPerThread; ++k) {
@@ -1619,6 +1624,12 @@ struct WsBlock {
     size_t bytes = 0;
     hipEvent_t ev = nullptr;       // recorded after the last user's kernels
     hipStream_t last = nullptr;    // the last user's stream
+    // Forward calls keep two work-list counter sets at the start of the
+    // block and use set gen % 2; each call's partition zeroes the other set
+    // for the next call.  primed: set gen % 2 is zero (the last user was a
+    // forward call whose partition was enqueued), so no clear is needed.
+    uint32_t gen = 0;
+    bool primed = false;
 };
 
 // Free blocks of one device, and the bytes of blocks that calls hold.
@@ -1654,6 +1665,7 @@ struct CallWorkspace {
     int dev = -1;
     Kind kind = NONE;
     WsBlock block;
+    bool keep_primed = false;  // set by a forward call once its partition is enqueued
     CallWorkspace() = default;
     CallWorkspace(const CallWorkspace&) = delete;
     CallWorkspace& operator=(const CallWorkspace&) = delete;
@@ -1673,6 +1685,7 @@ struct CallWorkspace {
                 return;
             }
             block.last = stream;
+            block.primed = keep_primed;
             std::vector<WsBlock> evict;
             {
                 std::lock_guard<std::mutex> lk(c.mu);
@@ -1962,7 +1975,7 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     // workspace: counters | medium rows | heavy rows | chunk items | partial (m,l) | partial acc
     const PartCaps caps = part_caps(a.E, heavy_min, chunk);
     size_t off = 0;
-    const size_t o_cnt = off;      off = align_up(off + kCntSetWords * sizeof(int32_t), 256);
+    const size_t o_cnt = off;      off = align_up(off + 2 * kCntSetWords * sizeof(int32_t), 256);  // two sets
     const size_t o_med = off;      off = align_up(off + (size_t)a.N * sizeof(int32_t), 256);
     const size_t o_heavy = off;    off = align_up(off + (size_t)caps.heavy * sizeof(HeavyRow), 256);
     const size_t o_chunks = off;   off = align_up(off + (size_t)caps.items * sizeof(ChunkItem), 256);
@@ -1979,13 +1992,20 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     gt_status st = call_workspace(a.noalloc, dev, ws_bytes, stream, cw);
     if (st != GT_SUCCESS) return st;
     char* ws = cw.ptr;
-    int32_t* counters = reinterpret_cast<int32_t*>(ws + o_cnt);
+    // Counter sets: a cached block alternates between its two (the partition
+    // zeroes the other one for the block's next call), so a block whose last
+    // user was a forward call needs no clear kernel; a new block, the
+    // scratch array and a captured stream clear the one set they use.
+    int32_t* cnt_base = reinterpret_cast<int32_t*>(ws + o_cnt);
+    const bool alternate = cw.kind == CallWorkspace::CACHED;
+    int32_t* counters = cnt_base + (alternate ? (cw.block.gen & 1u) * kCntSetWords : 0);
 
     // (the allocation-free entry point records no profiling events: creating
     // them is a runtime allocation)
     PhaseEvents ph;
     if (!a.noalloc && (he = ph.start(stream)) != hipSuccess) return hip_fail(he, "profiling events");
-    if ((he = clear_counters(counters, kCntSetWords, stream)) != hipSuccess) return hip_fail(he, "counter clear");
+    if (!(alternate && cw.block.primed) && (he = clear_counters(counters, kCntSetWords, stream)) != hipSuccess)
+        return hip_fail(he, "counter clear");
 
     PartParams pp;
     pp.rowptr = a.rowptr;
@@ -2007,7 +2027,12 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
         pp.win_flags = reinterpret_cast<uint8_t*>(ws + o_win);
         pp.tile_min = tile_min;
     }
+    if (alternate) pp.zero_next = cnt_base + ((cw.block.gen + 1u) & 1u) * kCntSetWords;
     if ((he = launch_partition(pp, stream)) != hipSuccess) return hip_fail(he, "partition launch");
+    if (alternate) {
+        ++cw.block.gen;
+        cw.keep_primed = true;
+    }
     ph.mark(1, stream);  // the attention phase includes the tile kernel
     if constexpr (kTileShape) {
         if (tiles) {

@@ -361,6 +361,46 @@ def test_workspace_reuse_growth_and_release():
     assert gate_error(b1, ref, absagg) <= TOL_F32
 
 
+def test_counter_sets_across_mixed_calls():
+    """A forward call on a reused workspace block skips the counter clear: it
+    uses one of the block's two counter sets, and its partition zeroes the
+    other for the block's next call.  Segment reductions in between use the
+    block their own way (the next forward clears again).  A sequence of
+    forward calls on two graphs, with split rows and with the dense-tile
+    path, interleaved with reductions, all on one stream with no
+    synchronisation, gives every forward result exactly as a call on its
+    own."""
+    import paper_2605_31500_amd as gtm
+    cases = []
+    for seed, n, dtype in ((31, 3000, "f32"), (32, 40_000, "f32"), (33, 4096, "bf16")):
+        if dtype == "bf16":  # dense 64-id blocks: the tile path
+            rp, ci = synth.sbm_graph(seed, n, 64, 4)
+        else:
+            rp, ci = synth.ragged_graph(seed, n, max_deg=40, hubs={3: n - 1, 7: n // 2})
+        Q, K, V = synth.features(seed, n, 2, 64, dtype)
+        want = run_gpu(rp, ci, Q, K, V, np.float32(0.2))
+        dev = [to_device(x) for x in (rp, ci, Q, K, V)]
+        cases.append((dev, want))
+    X = to_device(synth.features(34, 40_000, 1, 32, "f32")[0].reshape(40_000, 32))
+    red_out = torch.empty_like(X)
+    rp2, ci2 = cases[1][0][0], cases[1][0][1]
+    torch.cuda.synchronize()
+    gtm.gt_workspace_release()
+    order = [0, 1, 0, "r", 2, 1, 1, "r", "r", 0, 2, 2, 1]
+    outs = []
+    for k in order:
+        if k == "r":
+            gtm.gt_segment_reduce(rp2, ci2, X, red_out, None, op="min")
+            continue
+        dev, _ = cases[k]
+        o = torch.empty_like(dev[2])
+        gtm.gt_attn_fwd_ex(*dev, o, np.float32(0.2))
+        outs.append((k, o))
+    torch.cuda.synchronize()
+    for k, o in outs:
+        assert np.array_equal(to_host_f32(o), cases[k][1]), "call on graph %d differs" % k
+
+
 def test_calls_return_without_waiting_for_the_device():
     """A call enqueues its work and returns: behind a device-side sleep on its
     stream, five calls take a small fraction of the sleep on the host (freeing
