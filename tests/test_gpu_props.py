@@ -401,6 +401,39 @@ def test_counter_sets_across_mixed_calls():
         assert np.array_equal(to_host_f32(o), cases[k][1]), "call on graph %d differs" % k
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_regular_entry_point_replays_in_a_hip_graph(dtype):
+    """On a stream being captured, a call takes its workspace stream-ordered
+    (allocation and free become graph nodes) and clears its counters with the
+    fill kernel.  Captured once, the graph is replayed three times, with eager
+    work and synchronisations between the replays; every replay equals the
+    eager call bit for bit (split rows and, for bf16 2x64, dense tiles)."""
+    import paper_2605_31500_amd as gtm
+    if dtype == "bf16":
+        rowptr, colidx = synth.sbm_graph(72, 8192, 64, 4)
+        H, D = 2, 64
+    else:
+        rowptr, colidx = synth.ragged_graph(71, 20_000, max_deg=60, hubs={2: 19_999, 9: 5000}, self_loops=True)
+        H, D = 4, 32
+    N = rowptr.size - 1
+    Q, K, V = synth.features(71, N, H, D, dtype)
+    want = run_gpu(rowptr, colidx, Q, K, V, np.float32(0.2))
+    dev = [to_device(x) for x in (rowptr, colidx, Q, K, V)]
+    out = torch.empty_like(dev[2])
+    fwd = gtm.gt_attn_fwd if dtype == "f32" else gtm.gt_attn_fwd_bf16
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        fwd(*dev, out, np.float32(0.2), stream=s)
+    for _ in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host_f32(out), want)
+
+
 def test_calls_return_without_waiting_for_the_device():
     """A call enqueues its work and returns: behind a device-side sleep on its
     stream, five calls take a small fraction of the sleep on the host (freeing
