@@ -898,51 +898,65 @@ gt_tile_kernel(TileParams p) {
     const int srow = lane >> 2, sub = lane & 3;
     const int wrow = 16 * wv + srow;  // row within the window
     const int64_t r = r0 + wrow;
-    int64_t mb = 0, me = 0;
-    if (r < p.N) {
-        mb = p.rowptr[r];
-        me = p.rowptr[r + 1];
-    }
+    // (rows past the end read rowptr[N] twice: an empty row.  The loads of
+    // this stage are unconditional, with clamped addresses, so that the
+    // compiler can wait for the row bounds alone while the later staging loads
+    // are still in flight.)
+    const int64_t mb = p.rowptr[r < p.N ? r : p.N];
+    const int64_t me = p.rowptr[r + 1 < p.N ? r + 1 : p.N];
     if (!all_dense && !p.win_flags[blockIdx.x]) return;
 
-    // ---- 1. staging
-    if (tid <= kWin) lds.rp[tid] = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
-    for (int v = tid; v < kWin * (HD / 8); v += kBlock) {
+    // ---- 1. staging.  Every load of the stage is issued before any LDS write,
+    // with compile-time trip counts: the window's rowptr entries, its K and V
+    // pieces and this lane's strip row of Q go out together, then the entries
+    // of the mask stage (which wait only for the row bounds above), and only
+    // then do the LDS writes wait for their data.  So staging a window costs
+    // about two memory latencies (row bounds, then entries), not one per loop
+    // trip.
+    constexpr int kKPieces = kWin * (HD / 8);        // 16-byte pieces of the K tile
+    constexpr int kVPieces = (kWin / 2) * (HD / 8);  // pieces of the row pairs of the V tile
+    constexpr int kKIt = (kKPieces + kBlock - 1) / kBlock;
+    constexpr int kVIt = (kVPieces + kBlock - 1) / kBlock;
+    static_assert(kKPieces % kBlock == 0, "the K tile is a whole number of workgroup loads");
+    // Rows past the end read the last row instead: their K columns and Q rows
+    // are masked out of every score, and their V columns are zeroed when the
+    // tile is written (a weight of 0 must not meet a non-finite value).  No
+    // loaded register is overwritten before it arrives, which would make the
+    // load wait at once.
+    const int64_t last = p.N - 1;
+    const int64_t rpv = p.rowptr[(r0 + tid < p.N) ? r0 + tid : p.N];
+    uint4 kx[kKIt];
+#pragma unroll
+    for (int it = 0; it < kKIt; ++it) {
         // K rows as they are: 16 bytes of one row per lane
-        const int cc = v % kWin, e0 = (v / kWin) * 8;
-        uint4 kx = make_uint4(0, 0, 0, 0);
-        if (r0 + cc < p.N) kx = *reinterpret_cast<const uint4*>(p.K + ((r0 + cc) * HD + e0) * 2);
-        *reinterpret_cast<uint4*>(&lds.big.kv.k[cc][e0]) = kx;
+        const int v = tid + it * kBlock, cc = v % kWin, e0 = (v / kWin) * 8;
+        const int64_t rk = r0 + cc;
+        kx[it] = *reinterpret_cast<const uint4*>(p.K + ((rk < p.N ? rk : last) * HD + e0) * 2);
     }
-    for (int v = tid; v < (kWin / 2) * (HD / 8); v += kBlock) {
-        // V transposed: a lane takes 8 elements of two consecutive rows and writes
-        // each element pair as one dword, so the 32 lanes of a row pair write 32
-        // consecutive dwords of one vt row
+    uint4 va[kVIt], vb[kVIt];
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) {
+        // V transposed: a lane takes 8 elements of two consecutive rows (the
+        // 1x32 shape has fewer pieces than lanes: the rest load piece 0)
+        const int v0 = tid + it * kBlock;
+        const int v = (kVPieces % kBlock == 0 || v0 < kVPieces) ? v0 : 0;
         const int pc = v % (kWin / 2), e0 = (v / (kWin / 2)) * 8;
         const int64_t ra = r0 + 2 * pc;
-        uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
-        if (ra < p.N) va = *reinterpret_cast<const uint4*>(p.V + (ra * HD + e0) * 2);
-        if (ra + 1 < p.N) vb = *reinterpret_cast<const uint4*>(p.V + ((ra + 1) * HD + e0) * 2);
-        const uint32_t wa[4] = {va.x, va.y, va.z, va.w}, wb[4] = {vb.x, vb.y, vb.z, vb.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            *reinterpret_cast<uint32_t*>(&lds.big.kv.vt[e0 + 2 * q][2 * pc]) = pair_lo(wa[q], wb[q]);
-            *reinterpret_cast<uint32_t*>(&lds.big.kv.vt[e0 + 2 * q + 1][2 * pc]) = pair_hi(wa[q], wb[q]);
-        }
+        va[it] = *reinterpret_cast<const uint4*>(p.V + ((ra < p.N ? ra : last) * HD + e0) * 2);
+        vb[it] = *reinterpret_cast<const uint4*>(p.V + ((ra + 1 < p.N ? ra + 1 : last) * HD + e0) * 2);
     }
     // this lane's strip row of Q (all heads), as MFMA B operands
     const int64_t qrow = r0 + 16 * wv + n16;
     uint4 qreg[HD / 32];
 #pragma unroll
     for (int t = 0; t < HD / 32; ++t) {
-        qreg[t] = make_uint4(0, 0, 0, 0);
-        if (qrow < p.N) qreg[t] = *reinterpret_cast<const uint4*>(p.Q + (qrow * HD + 32 * t + 8 * g16) * 2);
+        qreg[t] = *reinterpret_cast<const uint4*>(p.Q + ((qrow < p.N ? qrow : last) * HD + 32 * t + 8 * g16) * 2);
     }
 
     // ---- 2. in-window masks: 4 lanes per row, 16 rows per wave.  The entries
-    // come straight from colidx (one batch of independent loads, overlapping
-    // the staging above); the remaining-entry stream reads them again later,
-    // so the window needs no LDS copy of its entries.
+    // come straight from colidx (one batch of independent loads, behind the
+    // staging loads); the remaining-entry stream reads them again later, so
+    // the window needs no LDS copy of its entries.
     const bool light = r < p.N && (me - mb) <= p.light_max;
     constexpr int kMaskPer = kWinMaxDeg / 4;  // entries per lane (light_max <= kWinMaxDeg)
     int32_t ent[kMaskPer] = {};
@@ -951,6 +965,30 @@ gt_tile_kernel(TileParams p) {
         for (int k = 0; k < kMaskPer; ++k) {
             const int64_t pos = mb + sub + 4 * k;
             ent[k] = p.colidx[pos < me ? pos : me - 1];
+        }
+    }
+    // the staged tiles to LDS (read after the barrier below)
+    if (tid <= kWin) lds.rp[tid] = rpv;
+#pragma unroll
+    for (int it = 0; it < kKIt; ++it) {
+        const int v = tid + it * kBlock, cc = v % kWin, e0 = (v / kWin) * 8;
+        *reinterpret_cast<uint4*>(&lds.big.kv.k[cc][e0]) = r0 + cc < p.N ? kx[it] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) {
+        // each element pair as one dword, so the 32 lanes of a row pair write 32
+        // consecutive dwords of one vt row
+        const int v = tid + it * kBlock, pc = v % (kWin / 2), e0 = (v / (kWin / 2)) * 8;
+        if (kVPieces % kBlock == 0 || v < kVPieces) {
+            const int64_t ra = r0 + 2 * pc;
+            const uint4 a = ra < p.N ? va[it] : make_uint4(0, 0, 0, 0);
+            const uint4 b = ra + 1 < p.N ? vb[it] : make_uint4(0, 0, 0, 0);
+            const uint32_t wa[4] = {a.x, a.y, a.z, a.w}, wb[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                *reinterpret_cast<uint32_t*>(&lds.big.kv.vt[e0 + 2 * q][2 * pc]) = pair_lo(wa[q], wb[q]);
+                *reinterpret_cast<uint32_t*>(&lds.big.kv.vt[e0 + 2 * q + 1][2 * pc]) = pair_hi(wa[q], wb[q]);
+            }
         }
     }
     uint64_t mk = 0;
