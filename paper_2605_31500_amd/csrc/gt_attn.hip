@@ -1119,26 +1119,29 @@ gt_tile_kernel(TileParams p) {
     int32_t* gtile = lds.big.rest.ctile[wv] + g * kWinMaxDeg;
     constexpr int kRowPer = (kWinMaxDeg + G - 1) / G;  // a light row: at most kWinMaxDeg entries
     constexpr int kPasses = 16 / P;
-    // The row vectors of the group's rows, from the strip's MFMA operands
-    // (lane 16*g16 + n16 of qreg[t] holds elements 32t + 8*g16 .. + 7 of strip
-    // row n16) by cross-lane moves, rather than a second read from memory.
+    // The row vector of the group's row of a pass, from the strip's MFMA
+    // operands (lane 16*g16 + n16 of qreg[t] holds elements 32t + 8*g16 .. + 7
+    // of strip row n16) by cross-lane moves, rather than a second read from
+    // memory.  Taken at the top of each pass, where every lane is active (a
+    // move reads zero from an inactive lane), with selects rather than
+    // branches.
     constexpr bool kQRegs = QFromOperands<H, D, KIND>::value;
-    uint4 qpass[kQRegs ? kPasses : 1][Gm::kNV];
-#pragma unroll
-    for (int pass = 0; pass < (kQRegs ? kPasses : 0); ++pass)
+    auto row_vector = [&](int pass, uint4 (&qp)[Gm::kNV]) {
 #pragma unroll
         for (int k = 0; k < Gm::kNV; ++k) {
             const int e0 = 8 * (lig + k * G);  // first element of this lane's piece
-            const int src = 16 * ((e0 % 32) / 8) + pass * P + g;
-            uint4 v = make_uint4(0, 0, 0, 0);
+            const int src = 16 * ((e0 % 32) / 8) + pass * P + g, tsel = e0 / 32;
+            uint32_t v[4] = {0, 0, 0, 0};
 #pragma unroll
             for (int t = 0; t < HD / 32; ++t) {
-                const uint4 x = make_uint4(__shfl((int)qreg[t].x, src), __shfl((int)qreg[t].y, src),
-                                           __shfl((int)qreg[t].z, src), __shfl((int)qreg[t].w, src));
-                if (t == e0 / 32) v = x;
+                const uint32_t x[4] = {(uint32_t)__shfl((int)qreg[t].x, src), (uint32_t)__shfl((int)qreg[t].y, src),
+                                       (uint32_t)__shfl((int)qreg[t].z, src), (uint32_t)__shfl((int)qreg[t].w, src)};
+#pragma unroll
+                for (int c = 0; c < 4; ++c) v[c] = tsel == t ? x[c] : v[c];
             }
-            qpass[pass][k] = v;
+            qp[k] = make_uint4(v[0], v[1], v[2], v[3]);
         }
+    };
     auto load_entries = [&](int pass, int32_t (&e)[kRowPer]) {
         const int sr = pass * P + g, wr = 16 * wv + sr;
         const int64_t eb = lds.rp[wr], ee = lds.rp[wr + 1];
@@ -1157,6 +1160,8 @@ gt_tile_kernel(TileParams p) {
 #pragma unroll
         for (int k = 0; k < kRowPer; ++k) re[k] = nxt[k];
         if (pass + 1 < kPasses) load_entries(pass + 1, nxt);
+        uint4 qp[Gm::kNV];
+        if constexpr (kQRegs) row_vector(pass, qp);
         const int sr = pass * P + g;
         if (!((light_bits >> (4 * sr)) & 1ull)) continue;
         const bool use_tile = dense && ((ok_bits >> (4 * sr)) & 1ull);
@@ -1164,7 +1169,7 @@ gt_tile_kernel(TileParams p) {
         const int64_t row = r0 + wr;
         RS st;
         if constexpr (kQRegs)
-            st.begin_loaded(qpass[pass]);
+            st.begin_loaded(qp);
         else
             st.begin(p.Q, row, lig);
         if (use_tile) {
