@@ -1489,26 +1489,35 @@ __global__ void __launch_bounds__(kBlock) gt_merge_kernel(MergeParams p) {
         float m = -INFINITY, l = 0.0f, acc[F];
 #pragma unroll
         for (int f = 0; f < F; ++f) acc[f] = 0.0f;
-        for (int c0 = 0; c0 < w.nch; c0 += kMergeBatch) {
-            float2 ml[kMergeBatch];
-            float a[kMergeBatch][F];
+        // a batch holds at most 64 accumulator floats per lane (wide rows take
+        // fewer chunks per batch)
+        constexpr int kB = 64 / F < kMergeBatch ? (64 / F > 1 ? 64 / F : 1) : kMergeBatch;
+        for (int c0 = 0; c0 < w.nch; c0 += kB) {
+            float2 ml[kB];
+            float a[kB][F];
 #pragma unroll
-            for (int u = 0; u < kMergeBatch; ++u) {
+            for (int u = 0; u < kB; ++u) {
                 const int64_t slot = w.base + (c0 + u < w.nch ? c0 + u : w.nch - 1);
                 ml[u] = p.part_ml[slot * H + head];
 #pragma unroll
                 for (int f = 0; f < F; ++f) a[u][f] = p.part_acc[slot * HD + f0 + f];
             }
+            // chunks past the row's last are merged into nothing (selects, not
+            // a loop exit, so that the batch's loads stay ahead of their use)
 #pragma unroll
-            for (int u = 0; u < kMergeBatch; ++u) {
-                if (c0 + u >= w.nch) break;
+            for (int u = 0; u < kB; ++u) {
+                const bool valid = c0 + u < w.nch;
                 const float mn = fmaxf(m, ml[u].x);
                 const float ca = (m == mn) ? 1.0f : fast_exp2(m - mn);
                 const float cb = (ml[u].x == mn) ? 1.0f : fast_exp2(ml[u].x - mn);
-                l = l * ca + ml[u].y * cb;
+                const float ln = l * ca + ml[u].y * cb;
+                l = valid ? ln : l;
 #pragma unroll
-                for (int f = 0; f < F; ++f) acc[f] = acc[f] * ca + a[u][f] * cb;
-                m = mn;
+                for (int f = 0; f < F; ++f) {
+                    const float an = acc[f] * ca + a[u][f] * cb;
+                    acc[f] = valid ? an : acc[f];
+                }
+                m = valid ? mn : m;
             }
         }
         const float inv = l > 0.0f ? 1.0f / l : 0.0f;

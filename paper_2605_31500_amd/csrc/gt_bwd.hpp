@@ -328,10 +328,13 @@ __global__ void __launch_bounds__(kBlock) gt_bwd_merge_kernel(BwdParams p) {
         float s1[F], s2[F];
 #pragma unroll
         for (int f = 0; f < F; ++f) s1[f] = s2[f] = 0.0f;
-        for (int c0 = 0; c0 < w.nch; c0 += kMergeBatch) {
-            float a1[kMergeBatch][F], a2[kMergeBatch][F];
+        // a batch holds at most 64 partial floats per lane
+        constexpr int kPer = (MODE ? 2 : 1) * F;
+        constexpr int kB = 64 / kPer < kMergeBatch ? (64 / kPer > 1 ? 64 / kPer : 1) : kMergeBatch;
+        for (int c0 = 0; c0 < w.nch; c0 += kB) {
+            float a1[kB][F], a2[kB][F];
 #pragma unroll
-            for (int u = 0; u < kMergeBatch; ++u) {
+            for (int u = 0; u < kB; ++u) {
                 const int64_t slot = w.base + (c0 + u < w.nch ? c0 + u : w.nch - 1);
                 const float* src = p.part + slot * NACC * HD + f0;
 #pragma unroll
@@ -340,13 +343,16 @@ __global__ void __launch_bounds__(kBlock) gt_bwd_merge_kernel(BwdParams p) {
                     a2[u][f] = MODE ? src[HD + f] : 0.0f;
                 }
             }
+            // chunks past the row's last add nothing (selects, not a loop exit,
+            // so that the batch's loads stay ahead of their use)
 #pragma unroll
-            for (int u = 0; u < kMergeBatch; ++u) {
-                if (c0 + u >= w.nch) break;
+            for (int u = 0; u < kB; ++u) {
+                const bool valid = c0 + u < w.nch;
 #pragma unroll
                 for (int f = 0; f < F; ++f) {
-                    s1[f] += a1[u][f];
-                    s2[f] += a2[u][f];
+                    const float t1 = s1[f] + a1[u][f], t2 = s2[f] + a2[u][f];
+                    s1[f] = valid ? t1 : s1[f];
+                    s2[f] = valid ? t2 : s2[f];
                 }
             }
         }

@@ -315,16 +315,26 @@ __global__ void __launch_bounds__(kBlock) gt_reduce_merge_kernel(ReduceParams p)
         uint64_t best[PER];
 #pragma unroll
         for (int q = 0; q < PER; ++q) best[q] = kRedEmpty;
-        for (int c = 0; c < w.nch; ++c) {
-            const uint64_t* src = p.part + (int64_t)(w.base + c) * F;
+        // kRB chunks per round (about 8 loads per lane in flight), loaded
+        // before any is compared; a round past the row's last chunk re-reads
+        // the last one, which leaves the minimum unchanged
+        constexpr int kRB = 8 / PER > 1 ? 8 / PER : 1;
+        for (int c0 = 0; c0 < w.nch; c0 += kRB) {
+            uint64_t v[kRB][PER];
 #pragma unroll
-            for (int q = 0; q < PER; ++q) {
-                const int f = lane + q * kWave;
-                if (f < F) {
-                    const uint64_t v = src[f];
-                    best[q] = v < best[q] ? v : best[q];
+            for (int u = 0; u < kRB; ++u) {
+                const int c = c0 + u < w.nch ? c0 + u : w.nch - 1;
+                const uint64_t* src = p.part + (int64_t)(w.base + c) * F;
+#pragma unroll
+                for (int q = 0; q < PER; ++q) {
+                    const int f = lane + q * kWave;
+                    v[u][q] = f < F ? src[f] : kRedEmpty;
                 }
             }
+#pragma unroll
+            for (int u = 0; u < kRB; ++u)
+#pragma unroll
+                for (int q = 0; q < PER; ++q) best[q] = v[u][q] < best[q] ? v[u][q] : best[q];
         }
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
