@@ -67,7 +67,11 @@ CAPTURES = {
 SQ_GROUP = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_INSTS_LDS", "SQ_INSTS_VALU", "SQ_INSTS_VMEM_RD",
             "SQ_WAVES", "GRBM_GUI_ACTIVE"]
 TA_GROUP = ["TA_TA_BUSY_sum", "TA_ADDR_STALLED_BY_TC_CYCLES_sum", "GRBM_GUI_ACTIVE"]
-COUNTER_GROUPS = [["FETCH_SIZE"], ["WRITE_SIZE"], ["TCC_HIT_sum", "TCC_MISS_sum"], SQ_GROUP, TA_GROUP]
+# vector L1: cycles stalled on data pending from L2, its requests to L2 and their summed latency
+# (cycles), for the misses it holds in flight (Little's law)
+TCP_GROUP = ["TCP_PENDING_STALL_CYCLES_sum", "TCP_TCC_READ_REQ_sum", "TCP_TCC_READ_REQ_LATENCY_sum",
+             "GRBM_GUI_ACTIVE"]
+COUNTER_GROUPS = [["FETCH_SIZE"], ["WRITE_SIZE"], ["TCC_HIT_sum", "TCC_MISS_sum"], SQ_GROUP, TA_GROUP, TCP_GROUP]
 COPY_MIB = 1024
 N_XCD, N_CU = 8, 256
 
@@ -221,6 +225,7 @@ def summarize(out, mode, source_hash):
     l2, _ = counters(d, ["TCC_HIT_sum", "TCC_MISS_sum"], kernels)
     sq, _ = counters(d, SQ_GROUP, kernels)
     ta, _ = counters(d, TA_GROUP, kernels)
+    tcp, _ = counters(d, TCP_GROUP, kernels)
     fb = fetch["FETCH_SIZE"] * 1024 * fscale
     wb = write["WRITE_SIZE"] * 1024 * wscale
     alg = live["roofline"]["algorithmic_bytes_per_launch"]
@@ -230,6 +235,10 @@ def summarize(out, mode, source_hash):
     conf = sq["SQ_LDS_BANK_CONFLICT"] / max(sq["SQ_LDS_IDX_ACTIVE"] - sq["SQ_LDS_BANK_CONFLICT"], 1.0)
     ta_cycles = ta["GRBM_GUI_ACTIVE"] / N_XCD
     ta_busy = ta["TA_TA_BUSY_sum"] / (N_CU * ta_cycles)  # one texture-address unit per CU
+    tcp_cycles = tcp["GRBM_GUI_ACTIVE"] / N_XCD
+    pending = tcp["TCP_PENDING_STALL_CYCLES_sum"] / (N_CU * tcp_cycles)  # one vector L1 per CU
+    l1_lat = tcp["TCP_TCC_READ_REQ_LATENCY_sum"] / max(tcp["TCP_TCC_READ_REQ_sum"], 1.0)
+    in_flight = tcp["TCP_TCC_READ_REQ_sum"] / (N_CU * tcp_cycles) * l1_lat
     kl = " + ".join("`%s`" % k[0] for k in main)
     L = ["# %s on %s" % (spec["title"], w), "",
          "Library sources (`paper_2605_31500_amd/csrc/*.hip`, `*.hpp`), sha256[:16] as computed by "
@@ -263,7 +272,12 @@ def summarize(out, mode, source_hash):
           "| texture-address unit busy | TA_TA_BUSY_sum %.3g / (%d CUs × GRBM_GUI_ACTIVE %.3g / %d XCDs) | %.1f %% |"
           % (ta["TA_TA_BUSY_sum"], N_CU, ta["GRBM_GUI_ACTIVE"], N_XCD, 100 * ta_busy),
           "| texture-address stalls on the cache | TA_ADDR_STALLED_BY_TC_CYCLES_sum / TA_TA_BUSY_sum | %.3f |"
-          % (ta["TA_ADDR_STALLED_BY_TC_CYCLES_sum"] / max(ta["TA_TA_BUSY_sum"], 1.0)), "",
+          % (ta["TA_ADDR_STALLED_BY_TC_CYCLES_sum"] / max(ta["TA_TA_BUSY_sum"], 1.0)),
+          "| vector L1 stalled on data pending from L2 | TCP_PENDING_STALL_CYCLES_sum %.3g / (%d CUs × cycles) | "
+          "%.1f %% |" % (tcp["TCP_PENDING_STALL_CYCLES_sum"], N_CU, 100 * pending),
+          "| L1 → L2 read latency | TCP_TCC_READ_REQ_LATENCY_sum / TCP_TCC_READ_REQ_sum (%.3g requests) | "
+          "%.0f cycles |" % (tcp["TCP_TCC_READ_REQ_sum"], l1_lat),
+          "| L1 misses in flight per CU (requests per CU-cycle × latency) | | %.0f |" % in_flight, "",
           "Algorithmic bytes per call (%s): %.4f GB; measured HBM / algorithmic = %.3f. FETCH_SIZE counts L2 "
           "misses sent to the fabric, which the 256 MB Infinity Cache may serve, so it bounds DRAM reads from "
           "above. The VALU share counts one wave-level VALU instruction per CU per cycle as the issue limit "
@@ -295,7 +309,9 @@ def summarize(out, mode, source_hash):
         with open(tf, "w") as f:
             json.dump(tj, f, indent=1, sort_keys=True)
     print("%-55s kernel %9.2f us  HBM %.3f GB  HBM/model %.3f  L2 hit %.3f  VALU %.2f  TA %.2f  LDS conflicts %.3f"
-          % (name, kavg, (fb + wb) / 1e9, (fb + wb) / alg, hit, valu, ta_busy, conf), flush=True)
+          "  L1 pending %.2f  in flight %.0f  latency %.0f"
+          % (name, kavg, (fb + wb) / 1e9, (fb + wb) / alg, hit, valu, ta_busy, conf, pending, in_flight, l1_lat),
+          flush=True)
     return name, entry
 
 

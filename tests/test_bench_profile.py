@@ -48,7 +48,11 @@ def capture(tmp_path, monkeypatch):
                                       "SQ_INSTS_VALU": 256.0 * 100, "SQ_INSTS_VMEM_RD": 5.0, "SQ_WAVES": 64.0,
                                       "GRBM_GUI_ACTIVE": 8 * 200.0},
               "_".join(bp.TA_GROUP): {"TA_TA_BUSY_sum": 256.0 * 150, "TA_ADDR_STALLED_BY_TC_CYCLES_sum": 100.0,
-                                      "GRBM_GUI_ACTIVE": 8 * 200.0}}
+                                      "GRBM_GUI_ACTIVE": 8 * 200.0},
+              # per CU: 100 of 200 cycles stalled; 0.5 requests per CU-cycle at 300 cycles each
+              "_".join(bp.TCP_GROUP): {"TCP_PENDING_STALL_CYCLES_sum": 256.0 * 100,
+                                       "TCP_TCC_READ_REQ_sum": 256.0 * 100, "TCP_TCC_READ_REQ_LATENCY_sum": 256.0 * 100 * 300,
+                                       "GRBM_GUI_ACTIVE": 8 * 200.0}}
     for g, vals in groups.items():
         write_csv(str(d / ("pmc_" + g) / "x_counter_collection.csv"), hdr,
                   counter_rows(k, vals) + counter_rows(other, {c: 1e9 for c in vals}))
@@ -73,6 +77,9 @@ def test_summary_arithmetic(capture):
     assert "| `gt_attn_kernel<float, 4, 32, 0>` | 10 | 200.00 |" in text
     assert "VALU issue share" in text and "| 50.0 % |" in text  # 25600 / (256 x 1600/8)
     assert "texture-address unit busy" in text and "| 75.0 % |" in text  # 38400 / (256 x 200)
+    assert "vector L1 stalled on data pending from L2" in text and "| 50.0 % |" in text
+    assert "| 300 cycles |" in text           # latency sum / requests
+    assert "| L1 misses in flight per CU (requests per CU-cycle × latency) | | 150 |" in text  # 0.5 x 300
     assert "-- python3 %s --steps 50" % bp.BENCH in text     # the program follows `--` directly
     assert "rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum" in text
 
