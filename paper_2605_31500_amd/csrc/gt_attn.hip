@@ -299,6 +299,18 @@ __device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
 __device__ __forceinline__ uint32_t pair_lo(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x05040100u); }
 __device__ __forceinline__ uint32_t pair_hi(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
 
+// Exponent-all-ones test of the eight bf16 values of v, folded into acc: a
+// half's masked exponent plus 0x80 reaches bit 15 only when all eight exponent
+// bits are set (Inf or NaN); the halves cannot carry into each other.  Any
+// such value made bit 15 or 31 of acc set.
+__device__ __forceinline__ uint32_t fold_nonfinite_bf16(uint32_t acc, const uint4& v) {
+    acc |= (v.x & 0x7F807F80u) + 0x00800080u;
+    acc |= (v.y & 0x7F807F80u) + 0x00800080u;
+    acc |= (v.z & 0x7F807F80u) + 0x00800080u;
+    acc |= (v.w & 0x7F807F80u) + 0x00800080u;
+    return acc;
+}
+
 // Orders LDS traffic of one wavefront around a tile hand-off (the hardware
 // executes a wave's LDS operations in order; this stops compiler reordering).
 __device__ __forceinline__ void wave_lds_fence() {
@@ -774,8 +786,8 @@ __global__ void __launch_bounds__(kBlock) gt_attn_kernel(AttnParams p) {
 //      LDS with independent loads, and each light row's entries in registers;
 //   2. per light row, a 64-bit mask of its in-window entries (a row with a
 //      repeated in-window entry cannot be a mask and does not use the tile);
-//   3. if the window holds at least `min_entries` masked entries, per head and
-//      per 16-row strip (one wave each):
+//   3. if the window holds at least `min_entries` masked entries and its V
+//      tile only finite values, per head and per 16-row strip (one wave each):
 //        S^T = K_w Q_strip^T  (bf16 MFMA 16x16x32, fp32 accumulate),
 //      masked row-wise softmax statistics, and acc = P V_w (MFMA with P as
 //      the sum of two bf16 terms, so the weights keep 16 significant bits;
@@ -796,6 +808,7 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kWin = 64;          // window rows = tile columns
 constexpr int kWinMaxDeg = 64;    // light rows handled here have at most this degree
+constexpr int kNoTile = -(1 << 28);  // a wave's window count that rules the tile out
 // Padded row of the transposed V tile, in bf16 elements: 34 dwords, so that
 // the 16 rows one P*V operand load reads (8 bytes per lane) start 2 banks
 // apart and cover all 32 banks once (a 36-dword row put rows n and n + 8 on
@@ -974,6 +987,11 @@ gt_tile_kernel(TileParams p) {
         const int v = tid + it * kBlock, cc = v % kWin, e0 = (v / kWin) * 8;
         *reinterpret_cast<uint4*>(&lds.big.kv.k[cc][e0]) = r0 + cc < p.N ? kx[it] : make_uint4(0, 0, 0, 0);
     }
+    // Inf or NaN anywhere in the value tile: P*V sums over every column of
+    // the window, and a weight of 0 times such a value is NaN, so one row's
+    // value would leak into rows that do not reference it.  Such a window is
+    // streamed instead (below).
+    uint32_t vbits = 0;
 #pragma unroll
     for (int it = 0; it < kVIt; ++it) {
         // each element pair as one dword, so the 32 lanes of a row pair write 32
@@ -983,6 +1001,7 @@ gt_tile_kernel(TileParams p) {
             const int64_t ra = r0 + 2 * pc;
             const uint4 a = ra < p.N ? va[it] : make_uint4(0, 0, 0, 0);
             const uint4 b = ra + 1 < p.N ? vb[it] : make_uint4(0, 0, 0, 0);
+            vbits = fold_nonfinite_bf16(fold_nonfinite_bf16(vbits, a), b);
             const uint32_t wa[4] = {a.x, a.y, a.z, a.w}, wb[4] = {b.x, b.y, b.z, b.w};
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -1012,7 +1031,10 @@ gt_tile_kernel(TileParams p) {
     int wc = (sub == 0 && tile_ok) ? cnt : 0;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) wc += __shfl_xor(wc, o);
-    if (lane == 0) lds.wave_cnt[wv] = wc;
+    // a wave that staged a non-finite value puts the window's count far below
+    // any threshold
+    const bool v_nonfinite = __ballot((vbits & 0x80008000u) != 0) != 0;
+    if (lane == 0) lds.wave_cnt[wv] = v_nonfinite ? kNoTile : wc;
     const uint64_t ok_bits = __ballot(sub == 0 && tile_ok);     // bit 4*sr: strip row sr
     const uint64_t light_bits = __ballot(sub == 0 && light);
     __syncthreads();
