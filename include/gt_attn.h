@@ -27,7 +27,9 @@
  *
  * Precision: loads fp32 or bf16 (bf16 is widened exactly), accumulates in
  * fp32, exponentials in base 2 on a log2(e)-prescaled score; bf16 outputs
- * are rounded to nearest even from the fp32 result.
+ * are rounded to nearest even from the fp32 result.  Inf and NaN in the K or
+ * V row of a node reach only the rows whose entries name that node (there
+ * the output is non-finite where the exact result is, elementwise for V).
  *
  * Ownership and memory: every pointer argument is DEVICE memory owned by the
  * caller; the library neither frees nor retains it past the enqueued work.
