@@ -33,6 +33,8 @@
  *
  * Ownership and memory: every pointer argument is DEVICE memory owned by the
  * caller; the library neither frees nor retains it past the enqueued work.
+ * A call works on the calling thread's current device: `stream` (0 for the
+ * null stream) must belong to it, else GT_ERROR_INVALID_VALUE.
  * `out` must not overlap Q, K or V.  Q, K, V and out must be 16-byte aligned.
  * Workspace (degree-bin lists, the light-row order of narrow-row shapes,
  * partial softmax states of split rows and the work-list counters) is owned

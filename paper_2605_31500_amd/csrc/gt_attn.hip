@@ -1962,6 +1962,25 @@ int default_chunk(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
     return (int)(c < kWave ? kWave : c);
 }
 
+// The device a call works on: the calling thread's current device.  The
+// workspace, its events and the kernels' memory all belong to it, so a stream
+// created on another device is refused rather than fed memory it may not be
+// able to reach.  (A stream handle the runtime cannot resolve is left to the
+// launch, which reports it.)
+gt_status call_device(hipStream_t stream, int* dev) {
+    hipError_t he = hipGetDevice(dev);
+    if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+    hipDevice_t sd = *dev;
+    if (hipStreamGetDevice(stream, &sd) != hipSuccess) {
+        (void)hipGetLastError();
+        return GT_SUCCESS;
+    }
+    if (sd != *dev)
+        return fail(GT_ERROR_INVALID_VALUE, "the stream belongs to device " + std::to_string(sd) +
+                                                ", the current device is " + std::to_string(*dev));
+    return GT_SUCCESS;
+}
+
 int device_cus(int dev) {
     static std::atomic<int> cache[64];
     if (dev < 0 || dev >= 64) return 256;
@@ -2028,8 +2047,8 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     if (tiles && light_max > kWinMaxDeg) light_max = kWinMaxDeg;
 
     int dev = 0;
-    hipError_t he = hipGetDevice(&dev);
-    if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+    if (const gt_status ds = call_device(stream, &dev); ds != GT_SUCCESS) return ds;
+    hipError_t he = hipSuccess;
     if (grid <= 0) {
         // About two light items (P rows each) per wave, between 4x and 64x the
         // number of workgroups the device holds at once: finer than one

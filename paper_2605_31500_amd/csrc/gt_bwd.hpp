@@ -1,6 +1,6 @@
 // Backward pass of the fused graph-transformer attention (included by
 // gt_attn.hip inside its anonymous namespace; uses its device helpers, the
-// degree partition kernel and the per-stream workspace cache).
+// degree partition kernel and the call workspace).
 //
 // Gradients for an upstream gradient dO (paper, Appendix D.2, backward pass of
 // the graph transformer: the weights are recomputed from the stored per-row
@@ -397,8 +397,8 @@ gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
     const int heavy_min = 256;
     const int chunk = default_chunk(a.E, 2 * Gm::kRowBytes, Gm::kP * Gm::kU);  // both passes gather two rows
     int dev = 0;
-    hipError_t he = hipGetDevice(&dev);
-    if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+    if (const gt_status ds = call_device(stream, &dev); ds != GT_SUCCESS) return ds;
+    hipError_t he = hipSuccess;
     const int64_t resident = (int64_t)device_cus(dev) * 4;
     const int64_t light_items = (a.N + Gm::kP - 1) / Gm::kP;
     int64_t g = light_items / (2 * kWavesPerBlock);

@@ -393,8 +393,8 @@ gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t st
     if (heavy_min <= light_max) heavy_min = light_max + 1;
 
     int dev = 0;
-    hipError_t he = hipGetDevice(&dev);
-    if (he != hipSuccess) return hip_fail(he, "hipGetDevice");
+    if (const gt_status ds = call_device(stream, &dev); ds != GT_SUCCESS) return ds;
+    hipError_t he = hipSuccess;
     if (grid <= 0) {
         const int64_t resident = (int64_t)device_cus(dev) * reduce_blocks_per_cu<T, NVEC>(dev);
         const int64_t light_items = (a.N + Gm::kP - 1) / Gm::kP;
