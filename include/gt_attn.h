@@ -123,16 +123,20 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  *   heavy_min_deg : rows of degree >= this are scheduled first; those longer
  *                   than one chunk are split into chunks processed by
  *                   different wavefronts and merged afterwards; rows in
- *                   between get one wavefront each (default 256)
+ *                   between get one wavefront each (default 256; on graphs
+ *                   whose default chunk exceeds 1024 and where a wavefront
+ *                   holds two or more rows, a quarter of that chunk, except
+ *                   for the GATv2 forward)
  *   chunk_edges   : CSR entries per chunk of a split row, rounded up to a
  *                   multiple of 64; a row is cut into at most 32 chunks, so
- *                   very long rows get longer chunks (default: 1024 on large
- *                   graphs, shorter on small ones, down to 64, so that one
- *                   chunk's chain of dependent steps stays within about half
- *                   the call's gather time; the graph size where 1024 is
- *                   reached depends on the bytes gathered per entry: the
- *                   graph-transformer forward on the arxiv-shaped 169K-node
- *                   fp32 4x32 graph gets 1024, the GATv2 forward 768)
+ *                   very long rows get longer chunks (default: from the
+ *                   call's gather time at about 7 TB/s and one microsecond
+ *                   per step: up to half of it in steps, at most 1024
+ *                   entries, down to 64 on small graphs; where an eighth of
+ *                   it exceeds 1024 entries, that eighth, up to 8192 (not for
+ *                   the GATv2 forward).  The graph-transformer forward gets
+ *                   1024 on the arxiv-shaped 169K-node fp32 4x32 graph and
+ *                   8192 on R-MAT scale 21; the GATv2 forward 768 and 1024)
  *   grid_blocks   : workgroups of the attention kernel, rounded up to a
  *                   multiple of 8 (default: about two light work items per
  *                   wavefront, within 4x..64x the resident workgroups)

@@ -1953,13 +1953,42 @@ PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
 // graph-transformer forward (two gathered rows per entry) the arxiv-shaped
 // 169K-node graph and every larger one get 1024; the GATv2 forward, one
 // gathered row per entry, gets 768 there and 1024 from about twice its size.
-int default_chunk(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
+double chunk_budget(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
     constexpr double kGatherBytesPerSecond = 7.0e12, kStepSeconds = 1.0e-6;
     const double gather_seconds = (double)E * (double)bytes_per_entry / kGatherBytesPerSecond;
-    const double entries = 0.5 * gather_seconds / kStepSeconds * entries_per_step;
+    return 0.5 * gather_seconds / kStepSeconds * entries_per_step;
+}
+
+int default_chunk(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
+    const double entries = chunk_budget(E, bytes_per_entry, entries_per_step);
     if (entries >= 1024.0) return 1024;
     const int64_t c = ((int64_t)entries + kWave - 1) / kWave * kWave;
     return (int)(c < kWave ? kWave : c);
+}
+
+// Chunks and front rows on large graphs (the graph-transformer forward, its
+// backward and the segment reduction; the GATv2 forward keeps the rule
+// above).  Where a chunk of an eighth of the gather time holds more than
+// 1024 entries, chunks take that length, up to 8192; and where a wave holds
+// two or more rows, only rows of at least a quarter chunk go first as front
+// rows, the others being medium rows of one wavefront each.  Measured per call
+// against 1024-entry chunks and a front threshold of 256: R-MAT scale 21 fp32
+// 4x32 6.528 -> 6.260 ms and bf16 3.103 -> 2.936 ms, the backward on the bf16
+// one 8.30 -> 7.97 ms, the 512-feature min on the fp32 one 14.45 -> 14.27 ms;
+// the arxiv-shaped power-law graph at 2.1M nodes about 1 % faster; the
+// lognormal-hub and SBM graphs level; graphs up to the 169K-node one keep
+// their chunks.  With one row per wave (lognormal hubs, 8x64 bf16) a front
+// threshold of 2048 cost 0.3-0.6 %, so those shapes keep 256.  (For the GATv2
+// score the same lengths made R-MAT bf16 1.5 % slower.)
+int default_chunk_long(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
+    const double quarter = 0.25 * chunk_budget(E, bytes_per_entry, entries_per_step);
+    if (quarter <= 1024.0) return default_chunk(E, bytes_per_entry, entries_per_step);
+    if (quarter >= 8192.0) return 8192;
+    return (int)(((int64_t)quarter + kWave - 1) / kWave * kWave);
+}
+
+int default_front(int chunk, int rows_per_wave) {
+    return rows_per_wave >= 2 && chunk / 4 > 256 ? chunk / 4 : 256;
 }
 
 // The device a call works on: the calling thread's current device.  The
@@ -2013,17 +2042,20 @@ gt_status launch(const Args& a, const gt_tuning* tu, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
     // Defaults chosen by measurement on the five workload shapes (power law,
     // R-MAT, SBM, lognormal hubs): a group handles rows of up to 8 steps;
-    // rows of degree >= 256 go first, split into chunks of 1024 entries on
-    // large graphs, shorter ones on small graphs (default_chunk).  GATv2
+    // rows of degree >= 256 go first, split into chunks of up to 1024
+    // entries, shorter ones on small graphs (default_chunk); on large graphs
+    // longer chunks and, where a wave holds several rows, a higher front
+    // threshold (default_chunk_long, default_front).  GATv2
     // counts its own single gather per entry but the graph-transformer step:
     // that put its chunks at the measured optimum on the arxiv-shaped graph
     // with 16K and 65K nodes (65K: 92.6 -> 77.5 us per call) and at 768
     // entries on the 169K-node one (within 1 % of 1024).  Its own half step
     // would give 384 entries there, 5.7 % slower.
     int light_max = 8 * Gm::kU;
-    int heavy_min = 256;
-    int chunk = default_chunk(a.E, (KIND != KIND_GATV2 ? 2 : 1) * Gm::kRowBytes,
-                              Gm::kP * StepOf<T, H, D, KIND_GT>::value);
+    int chunk = KIND != KIND_GATV2
+                    ? default_chunk_long(a.E, 2 * Gm::kRowBytes, Gm::kP * StepOf<T, H, D, KIND_GT>::value)
+                    : default_chunk(a.E, Gm::kRowBytes, Gm::kP * StepOf<T, H, D, KIND_GT>::value);
+    int heavy_min = KIND != KIND_GATV2 ? default_front(chunk, Gm::kP) : 256;
     int grid = 0;
     // Dense-tile windows (tile shapes only): on by default, for windows
     // estimated to hold at least 256 in-window entries, which a 64-row block

@@ -394,8 +394,8 @@ template <typename T, int H, int D>
 gt_status launch_bwd(const BwdArgs& a, hipStream_t stream) {
     using Gm = Geo<T, H, D>;
     const int light_max = 8 * Gm::kU;
-    const int heavy_min = 256;
-    const int chunk = default_chunk(a.E, 2 * Gm::kRowBytes, Gm::kP * Gm::kU);  // both passes gather two rows
+    const int chunk = default_chunk_long(a.E, 2 * Gm::kRowBytes, Gm::kP * Gm::kU);  // both passes gather two rows
+    const int heavy_min = default_front(chunk, Gm::kP);
     int dev = 0;
     if (const gt_status ds = call_device(stream, &dev); ds != GT_SUCCESS) return ds;
     hipError_t he = hipSuccess;

@@ -381,8 +381,8 @@ template <typename T, int NVEC>
 gt_status launch_reduce(const ReduceArgs& a, const gt_tuning* tu, hipStream_t stream) {
     using Gm = RedGeo<T, NVEC>;
     int light_max = 8 * Gm::kU;
-    int heavy_min = 256;
-    int chunk = default_chunk(a.E, Gm::kRowBytes, Gm::kP * Gm::kU);
+    int chunk = default_chunk_long(a.E, Gm::kRowBytes, Gm::kP * Gm::kU);
+    int heavy_min = default_front(chunk, Gm::kP);
     int grid = 0;
     if (tu) {
         if (tu->light_max_deg > 0) light_max = tu->light_max_deg;
