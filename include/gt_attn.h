@@ -134,9 +134,10 @@ gt_status gt_attn_fwd_bf16(const int64_t* rowptr, const int32_t* colidx, const u
  *                   per step: up to half of it in steps, at most 1024
  *                   entries, down to 64 on small graphs; where an eighth of
  *                   it exceeds 1024 entries, that eighth, up to 8192 (not for
- *                   the GATv2 forward).  The graph-transformer forward gets
- *                   1024 on the arxiv-shaped 169K-node fp32 4x32 graph and
- *                   8192 on R-MAT scale 21; the GATv2 forward 768 and 1024)
+ *                   the GATv2 forward).  With fp32 4x32 features the
+ *                   graph-transformer forward gets 1024 on the arxiv-shaped
+ *                   169K-node graph and 8192 on R-MAT scale 21; the GATv2
+ *                   forward 768 and 1024)
  *   grid_blocks   : workgroups of the attention kernel, rounded up to a
  *                   multiple of 8 (default: about two light work items per
  *                   wavefront, within 4x..64x the resident workgroups)
