@@ -1949,10 +1949,10 @@ PartCaps part_caps(int64_t E, int heavy_min, int chunk) {
 // fp32 4x32 features, 16K nodes took 76 us per call at 1024 against 48 us at
 // 256, and 65K nodes 114 us against 95 us at 512.  The default keeps a chunk's
 // steps within half the time the call's gathers take at ~7 TB/s, in multiples
-// of 64, capped at 1024, the measured best on large graphs.  With the
-// graph-transformer forward (two gathered rows per entry) the arxiv-shaped
-// 169K-node graph and every larger one get 1024; the GATv2 forward, one
-// gathered row per entry, gets 768 there and 1024 from about twice its size.
+// of 64, capped at 1024 (longer chunks on large graphs: default_chunk_long
+// below).  With the graph-transformer forward (two gathered rows per entry)
+// the arxiv-shaped 169K-node graph gets 1024; the GATv2 forward, one gathered
+// row per entry, gets 768 there and 1024 from about twice its size.
 double chunk_budget(int64_t E, int64_t bytes_per_entry, int entries_per_step) {
     constexpr double kGatherBytesPerSecond = 7.0e12, kStepSeconds = 1.0e-6;
     const double gather_seconds = (double)E * (double)bytes_per_entry / kGatherBytesPerSecond;
