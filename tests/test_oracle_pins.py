@@ -242,3 +242,50 @@ def test_rejects_invalid_csr():
     with pytest.raises(ValueError):
         run(np.array([0, 2, 2], dtype=np.int64), np.array([0, 1, 1], dtype=np.int32), Q, K, V,
             np.float32(1.0))
+
+
+def dense_lse(rowptr, colidx, Qf, Kf, scale):
+    """ln sum over the row's entries (with multiplicity) of exp(score), from the
+    dense masked score matrix; -inf for an empty row."""
+    N, H, D = Qf.shape
+    C = np.zeros((N, N))
+    for i in range(N):
+        for e in range(rowptr[i], rowptr[i + 1]):
+            C[i, colidx[e]] += 1.0
+    out = np.full((N, H), -np.inf)
+    for h in range(H):
+        S = float(scale) * (Qf[:, h, :].astype(np.float64) @ Kf[:, h, :].astype(np.float64).T)
+        for i in range(N):
+            m = C[i] > 0
+            if m.any():
+                s = S[i, m]
+                mx = s.max()
+                out[i, h] = mx + math.log(float((C[i, m] * np.exp(s - mx)).sum()))
+    return out
+
+
+@pytest.mark.parametrize("case", range(60))
+def test_dense_form_on_random_small_graphs(case):
+    """Sixty seeded random cases of every size the oracle takes (1..40 rows, any
+    H and D, empty rows, repeats, self-loops, unsorted rows, hubs, scales from
+    negative to large), each against the dense masked form and its log-sum-exp."""
+    rng = np.random.default_rng(5000 + case)
+    N = int(rng.integers(1, 41))
+    H, D = int(rng.integers(1, 4)), int(rng.integers(1, 17))
+    dtype = "f32" if case % 2 == 0 else "bf16"
+    hubs = {int(rng.integers(0, N)): int(rng.integers(1, N))} if N >= 2 and case % 3 == 0 else None
+    rowptr, colidx = synth.ragged_graph(6000 + case, N, max_deg=int(rng.integers(0, 12)),
+                                        empty_frac=float(rng.choice([0.0, 0.2, 0.6])), hubs=hubs,
+                                        self_loops=bool(case % 4 == 1), dup_frac=float(rng.choice([0.0, 0.3])),
+                                        shuffle=bool(case % 5 == 2))
+    Q, K, V = synth.features(7000 + case, N, H, D, dtype, std=float(rng.choice([0.5, 1.0, 3.0])))
+    scale = np.float32(rng.choice([1 / math.sqrt(D), 0.0, -0.7, 4.0]))
+    out, absagg, lse = run(rowptr, colidx, Q, K, V, scale)
+    f = (lambda a: a) if dtype == "f32" else bf16_bits_to_f32
+    ref = dense_reference(rowptr, colidx, f(Q), f(K), f(V), scale)
+    np.testing.assert_allclose(out, ref, rtol=1e-10, atol=1e-10)
+    ref_lse = dense_lse(rowptr, colidx, f(Q), f(K), scale)
+    fin = np.isfinite(ref_lse)
+    assert np.array_equal(np.isneginf(lse), ~fin)
+    np.testing.assert_allclose(lse[fin], ref_lse[fin], rtol=1e-12, atol=1e-10)
+    assert np.all(absagg >= np.abs(out) - 1e-12)
