@@ -100,3 +100,25 @@ def test_permutation_invariance():
     b, _, lb = oracle.gatv2_fwd(rowptr, shuffled, Lf, Rf, att, 0.2)
     np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-13)
     np.testing.assert_allclose(la, lb, rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_dense_form_on_random_small_graphs(case):
+    """Forty seeded random cases (1..30 rows, any H and D, empty rows, repeats,
+    self-loops, unsorted rows, slopes from -1 to 3, attention vectors of
+    several scales) against the dense masked form."""
+    rng = np.random.default_rng(8000 + case)
+    N = int(rng.integers(1, 31))
+    H, D = int(rng.integers(1, 4)), int(rng.integers(1, 13))
+    dtype = "f32" if case % 2 == 0 else "bf16"
+    rowptr, colidx = synth.ragged_graph(8100 + case, N, max_deg=int(rng.integers(0, 10)),
+                                        empty_frac=float(rng.choice([0.0, 0.3])), self_loops=bool(case % 3 == 0),
+                                        dup_frac=float(rng.choice([0.0, 0.3])), shuffle=bool(case % 4 == 1))
+    Lf, Rf, _ = synth.features(8200 + case, N, H, D, dtype)
+    att = synth.normal(8300 + case, synth.STREAM_EXTRA + 9, (H, D), float(rng.choice([0.3, 1.0, 3.0])), "f32")
+    slope = float(rng.choice([0.2, 0.0, 1.0, -1.0, 3.0]))
+    out, absagg, _ = oracle.gatv2_fwd(rowptr, colidx, Lf, Rf, att, slope)
+    f = (lambda a: a) if dtype == "f32" else bf16_bits_to_f32
+    ref = dense_gatv2(rowptr, colidx, f(Lf), f(Rf), att, np.float32(slope))
+    np.testing.assert_allclose(out, ref, rtol=1e-10, atol=1e-10)
+    assert np.all(absagg >= np.abs(out) - 1e-12)

@@ -148,3 +148,25 @@ def test_rows_subset_matches_all_rows():
     rows = np.array([69, 3, 3, 0, 41], np.int64)
     o2, a2 = oracle.segment_reduce(rowptr, colidx, X, "max", rows=rows)
     assert np.array_equal(o2, out[rows]) and np.array_equal(a2, arg[rows])
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_brute_force_on_random_small_graphs(case):
+    """Forty seeded random cases (1..40 rows, 1..20 features, empty rows,
+    repeats, self-loops, unsorted rows, small-integer values with many ties)
+    against the brute force, min and max."""
+    rng = np.random.default_rng(9000 + case)
+    N, F = int(rng.integers(1, 41)), int(rng.integers(1, 21))
+    rowptr, colidx = synth.ragged_graph(9100 + case, N, max_deg=int(rng.integers(0, 12)),
+                                        empty_frac=float(rng.choice([0.0, 0.3])), self_loops=bool(case % 3 == 0),
+                                        dup_frac=float(rng.choice([0.0, 0.3])), shuffle=bool(case % 4 == 1))
+    if case % 2 == 0:
+        X = synth.normal(9200 + case, synth.STREAM_Q, (N, F), 1.0, "f32")
+        X[X == 0] = 0.5
+    else:
+        X = (rng.integers(1, 5, size=(N, F)) * rng.choice([-1.0, 1.0], size=(N, F))).astype(np.float32)
+    for op in ("min", "max"):
+        out, arg = oracle.segment_reduce(rowptr, colidx, X, op)
+        ref_out, ref_arg = brute(rowptr, colidx, X, op)
+        assert np.array_equal(bits_of(out), bits_of(ref_out))
+        assert np.array_equal(arg, ref_arg)
