@@ -101,3 +101,52 @@ def test_subsets_match_full_and_scales_bound():
     assert np.array_equal(sk, dK[rows]) and np.array_equal(sv, dV[rows])
     for g, sg in ((dQ, sdQ), (dK, sdK), (dV, sdV)):
         assert np.all(sg >= np.abs(g) * (1 - 1e-12))
+
+
+def dense_grads(rowptr, colidx, Qf, Kf, Vf, dOf, scale):
+    """Gradients of sum(out * dO) from the dense masked form by matrix calculus,
+    written independently of the oracle: per head, P = row-normalised
+    C * exp(S) with S = scale Q K^T and C the entry multiplicities;
+    dV = P^T dO, dS = P * (dO V^T - rowsum(P * dO V^T)), dQ = scale dS K,
+    dK = scale dS^T Q."""
+    N, H, D = Qf.shape
+    C = np.zeros((N, N))
+    for i in range(N):
+        for e in range(rowptr[i], rowptr[i + 1]):
+            C[i, colidx[e]] += 1.0
+    dQ, dK, dV = np.zeros((N, H, D)), np.zeros((N, H, D)), np.zeros((N, H, D))
+    for h in range(H):
+        q, k, v, do = (x[:, h, :].astype(np.float64) for x in (Qf, Kf, Vf, dOf))
+        S = float(scale) * (q @ k.T)
+        S = np.where(C > 0, S, -np.inf)
+        mx = S.max(axis=1, keepdims=True)
+        W = np.where(C > 0, C * np.exp(S - np.where(np.isfinite(mx), mx, 0.0)), 0.0)
+        Z = W.sum(axis=1, keepdims=True)
+        P = W / np.where(Z > 0, Z, 1.0)
+        dV[:, h, :] = P.T @ do
+        dP = do @ v.T
+        dS = P * (dP - (P * dP).sum(axis=1, keepdims=True))
+        dQ[:, h, :] = float(scale) * (dS @ k)
+        dK[:, h, :] = float(scale) * (dS.T @ q)
+    return dQ, dK, dV
+
+
+@pytest.mark.parametrize("case", range(30))
+def test_dense_gradients_on_random_small_graphs(case):
+    """Thirty seeded random cases (1..30 rows, any H and D, empty rows, repeats,
+    self-loops, unsorted rows, fp32 and bf16) against the dense gradients."""
+    rng = np.random.default_rng(10_000 + case)
+    N = int(rng.integers(1, 31))
+    H, D = int(rng.integers(1, 4)), int(rng.integers(1, 13))
+    dtype = "f32" if case % 2 == 0 else "bf16"
+    rowptr, colidx = synth.ragged_graph(10_100 + case, N, max_deg=int(rng.integers(0, 10)),
+                                        empty_frac=float(rng.choice([0.0, 0.3])), self_loops=bool(case % 3 == 0),
+                                        dup_frac=float(rng.choice([0.0, 0.3])), shuffle=bool(case % 4 == 1))
+    Q, K, V = synth.features(10_200 + case, N, H, D, dtype)
+    dO, _, _ = synth.features(10_300 + case, N, H, D, dtype)
+    scale = np.float32(rng.choice([1 / math.sqrt(D), -0.5, 2.0]))
+    dQ, dK, dV, _, _, _ = all_grads(rowptr, colidx, Q, K, V, dO, scale)
+    f = (lambda a: a) if dtype == "f32" else (lambda b: (np.asarray(b).astype(np.uint32) << 16).view(np.float32))
+    rQ, rK, rV = dense_grads(rowptr, colidx, f(Q), f(K), f(V), f(dO), scale)
+    for got, want in ((dQ, rQ), (dK, rK), (dV, rV)):
+        np.testing.assert_allclose(got, want, rtol=1e-9, atol=1e-10 * max(1.0, np.abs(want).max()))
