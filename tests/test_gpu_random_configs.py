@@ -3,8 +3,8 @@ repeated and unsorted entries, empty rows; 64-id block models that tile)
 crossed with random shapes, dtypes and partition settings (light bound, front
 threshold, chunk length, grid size, dense-tile threshold, weight precision),
 each against the float64 oracle (output and lse) and repeated bit for bit:
-the graph-transformer forward, the GATv2 forward and the segment min/max
-(bit-exact).  The cases are drawn from fixed seeds, so every run checks the
+the graph-transformer forward, the GATv2 forward, the segment min/max
+(bit-exact) and the backward.  The cases are drawn from fixed seeds, so every run checks the
 same ones."""
 import math
 
@@ -137,3 +137,22 @@ def test_random_case_segment_reduce(seed):
     ref, ref_arg = oracle.segment_reduce(rowptr, colidx, X, op)
     assert np.array_equal(bits, oracle_bits(ref, c["dtype"])), c
     assert np.array_equal(arg, ref_arg), c
+
+
+@pytest.mark.parametrize("seed", range(N_CASES // 4))
+def test_random_case_backward(seed):
+    """The backward on the same random graphs and shapes (its partition uses
+    the defaults; the forward that produces out and lse takes the case's
+    settings), each gradient against the oracle's under the gate."""
+    from tests.helpers import run_gpu_fwd_bwd
+    from tests.test_gpu_bwd import check_grads, check_lse
+    c = draw_case(30_000 + seed)
+    rowptr, colidx = make_graph(11_000 + seed, c["graph"])
+    N = rowptr.size - 1
+    Q, K, V = synth.features(12_000 + seed, N, c["H"], c["D"], c["dtype"], std=c["std"])
+    dO, _, _ = synth.features(13_000 + seed, N, c["H"], c["D"], c["dtype"])
+    scale = np.float32(1 / math.sqrt(c["D"]))
+    got = run_gpu_fwd_bwd(rowptr, colidx, Q, K, V, dO, scale, tuning=c["tuning"])
+    _, _, ref_lse = oracle.gt_attn_fwd(rowptr, colidx, Q, K, V, scale)
+    check_lse(got[1], ref_lse, 1e-5)
+    check_grads(rowptr, colidx, Q, K, V, dO, scale, got, c["dtype"])
