@@ -2,9 +2,9 @@
 repeated and unsorted entries, empty rows; 64-id block models that tile)
 crossed with random shapes, dtypes and partition settings (light bound, front
 threshold, chunk length, grid size, dense-tile threshold, weight precision),
-each against the float64 oracle (output and lse) and repeated bit for bit:
-the graph-transformer forward, the GATv2 forward, the segment min/max
-(bit-exact) and the backward.  The cases are drawn from fixed seeds, so every run checks the
+each against the float64 oracle: the graph-transformer forward and the GATv2
+forward (output and lse, and a second call bit for bit), the segment min/max
+(bit-exact) and the backward (lse and the three gradients).  The cases are drawn from fixed seeds, so every run checks the
 same ones."""
 import math
 
