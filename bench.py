@@ -220,14 +220,17 @@ def run_study(args, gt, torch, to_device, synth) -> int:
     return 0
 
 
+# All three with the dense tiles off, so that the partition alone is compared
+# (with the tiles on, bf16 rows of up to 64 entries would stay light in every
+# mode: the tile path caps the light bound).
 ABLATION_MODES = {
     # the default degree-aware partition
-    "degree_aware": None,
+    "degree_aware": {"dense_tiles": -1},
     # degree-agnostic: every row on one lane group, no split (one sub-wavefront per node)
-    "group_per_row": {"light_max_deg": 1 << 30, "heavy_min_deg": (1 << 30) + 1},
+    "group_per_row": {"light_max_deg": 1 << 30, "heavy_min_deg": (1 << 30) + 1, "dense_tiles": -1},
     # degree-agnostic: every row of degree >= 2 on one wavefront, no split
     # (the tuning interface keeps rows of degree <= 1 on lane groups)
-    "wave_per_row": {"light_max_deg": 1, "heavy_min_deg": 1 << 30},
+    "wave_per_row": {"light_max_deg": 1, "heavy_min_deg": 1 << 30, "dense_tiles": -1},
 }
 
 
